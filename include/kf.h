@@ -1,0 +1,177 @@
+/*
+ * kf.h -- C ABI of the weightless attention node's decode hot path on MI355X
+ * (gfx950): tail append, local partial attention over token-range routes,
+ * and the log-sum-exp merge of partials.
+ *
+ * Source: KernelFlume (arXiv 2606.29207).  Section 3.2 (Workflow of Elastic
+ * Decoding), steps 3 and 4; Section 4.1 (Elastic Communication: the routing
+ * table from token ranges to the nodes that hold them, one live tail per
+ * request); Section 5.1 (Query-First Attention: the tail appends before it
+ * attends, and the merge of partials equals attention over the whole range).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - All array pointers are DEVICE pointers owned by the caller; shape
+ *    structs are host pointers.  The library allocates and frees nothing.
+ *  - Every call is asynchronous on `stream` (a hipStream_t; NULL = the null
+ *    stream) and returns once its kernels are enqueued.
+ *  - Host-checkable problems (null pointers, misalignment, unsupported
+ *    shapes, a workspace that is too small) return a negative status before
+ *    anything is launched.
+ *  - Problems only the device can see (inconsistent route rows, page ids
+ *    outside the pool, a full tail) OR a KF_EFLAG_* bit into *err_flags (a
+ *    device int32 the caller zeroes and reads after synchronising).  Outputs
+ *    of an affected route or sequence are NaN; an append that fails leaves the
+ *    pools and the route unchanged.  Nothing is ever read or written outside
+ *    the arrays described here.
+ *  - Calls that share buffers must be ordered on one stream: within a decode
+ *    step, kf_kv_append -> kf_partial_attn -> kf_merge_partials.
+ *
+ * Storage formats
+ * ---------------
+ *  page    = 16 consecutive tokens of one route; head_dim = 128.
+ *  K pool  [num_pages][num_kv_heads][16 slots][128] elements (token-major)
+ *  V pool  [num_pages][num_kv_heads][128][16 slots] elements (dim-major)
+ *  element = bfloat16 (KF_KV_BF16) or OCP E4M3FN code (KF_KV_FP8_E4M3);
+ *            fp8 pools carry k_scale/v_scale [num_pages][num_kv_heads] float32
+ *            and an element's value is decode(code) * scale.
+ *  q       [num_seqs][num_q_heads][128] bfloat16; query head h reads KV head
+ *            h / (num_q_heads / num_kv_heads).
+ *  route r covers logical tokens [tok_begin, tok_end) of sequence `seq`;
+ *            local index j = t - tok_begin lives in page
+ *            page_ids[page_base + j / 16], slot j % 16.  Routes must not share
+ *            pages.  Routes of sequence b are rows
+ *            seq_route_begin[b] .. seq_route_begin[b+1]-1.
+ */
+#ifndef KF_H
+#define KF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KF_PAGE_SIZE 16
+#define KF_HEAD_DIM 128
+#define KF_MAX_GROUP 16 /* num_q_heads / num_kv_heads may not exceed this */
+
+/* One entry of the routing table (Section 4.1), single-GPU form: a token
+ * range of one request and the pages that hold it.  `part` names the
+ * partition (attention node) that owns the range; kernels do not read it. */
+typedef struct {
+  int32_t seq;       /* sequence index in [0, num_seqs) */
+  int32_t part;      /* owning partition id (informational) */
+  int32_t tok_begin; /* first logical token of the range */
+  int32_t tok_end;   /* one past the last resident token; the tail grows it */
+  int32_t page_base; /* index in page_ids of the range's first page */
+  int32_t page_cap;  /* pages reserved: page_ids[page_base .. page_base+page_cap) */
+} kf_route;
+
+typedef struct {
+  int32_t num_seqs;     /* B */
+  int32_t num_q_heads;  /* Hq, a multiple of num_kv_heads */
+  int32_t num_kv_heads; /* Hkv */
+  int32_t head_dim;     /* must be KF_HEAD_DIM */
+  int32_t page_size;    /* must be KF_PAGE_SIZE */
+  int32_t kv_dtype;     /* KF_KV_BF16 or KF_KV_FP8_E4M3 */
+  int32_t num_pages;    /* pages in each of the K and V pools (>= 1) */
+  int32_t num_page_ids; /* entries of page_ids */
+  float scale;          /* softmax scale applied to q.k, e.g. 1/sqrt(128) */
+} kf_shape;
+
+enum {
+  KF_OK = 0,
+  KF_ERR_INVALID_ARG = -1, /* null/misaligned pointer or inconsistent sizes */
+  KF_ERR_UNSUPPORTED = -2, /* a shape or dtype this build does not handle */
+  KF_ERR_WORKSPACE = -3,   /* workspace missing or smaller than required */
+  KF_ERR_HIP = -4          /* the HIP runtime refused a launch */
+};
+
+enum { KF_KV_BF16 = 0, KF_KV_FP8_E4M3 = 1 };
+
+enum {
+  KF_EFLAG_TAIL_FULL = 1, /* tail has no reserved page for the new token */
+  KF_EFLAG_BAD_ROUTE = 2, /* route row / tail index / CSR row inconsistent */
+  KF_EFLAG_BAD_PAGE = 4   /* a page id lies outside [0, num_pages) */
+};
+
+/*
+ * kf_kv_append -- tail append (Section 3.2, step 3; Section 5.1).
+ * For every sequence b with r = tail_route[b] >= 0: write k_new[b][g][:] and
+ * v_new[b][g][:] (bfloat16 [num_seqs][num_kv_heads][128]) for all KV heads g
+ * at local index j = routes[r].tok_end - routes[r].tok_begin of route r, then
+ * set routes[r].tok_end += 1.  tail_route[b] = -1 marks a sequence without
+ * an append this step.  Device checks (flag, no write): r < num_routes,
+ * routes[r].seq == b, tok_end >= tok_begin, j/16 < page_cap
+ * (KF_EFLAG_TAIL_FULL otherwise), page_base + j/16 < num_page_ids, page id in
+ * the pool.  Only bf16 pools are supported (KF_ERR_UNSUPPORTED for fp8).
+ * Alignment: every pointer 4-byte aligned.
+ */
+int kf_kv_append(const kf_shape* shape, void* k_pool, void* v_pool,
+                 const void* k_new, const void* v_new, kf_route* routes,
+                 int32_t num_routes, const int32_t* tail_route,
+                 const int32_t* page_ids, int32_t* err_flags, void* stream);
+
+/*
+ * kf_partial_attn_workspace_bytes -- device scratch kf_partial_attn needs for
+ * `num_routes` routes of at most `max_pages_per_route` pages each.  The
+ * workspace must be zero-filled before its first use; every call leaves its
+ * counter area zero again, so it can be reused across calls and steps.
+ * Returns 0 for invalid arguments.
+ */
+size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes,
+                                       int32_t max_pages_per_route);
+
+/*
+ * kf_partial_attn -- local core attention of every route (Section 3.2,
+ * step 3): for route r of sequence b and query head h,
+ *   s_t = scale * (q[b][h] . k_t) over the route's resident tokens t,
+ *   o_part[r][h][:] = sum_t softmax(s)_t v_t     (float32, normalised)
+ *   lse_part[r][h]  = ln sum_t exp(s_t)          (float32, natural log)
+ * An empty route (tok_end == tok_begin) gives o = 0, lse = -inf.
+ * Device checks (NaN outputs + KF_EFLAG_BAD_ROUTE): 0 <= seq < num_seqs,
+ * tok_end >= tok_begin, page_base >= 0, pages <= page_cap,
+ * pages <= max_pages_per_route, page_base + pages <= num_page_ids; a page id
+ * outside the pool gives NaN + KF_EFLAG_BAD_PAGE.
+ * k_scale/v_scale: NULL for bf16 pools, required for fp8 pools.
+ * o_part [num_routes][num_q_heads][128], lse_part [num_routes][num_q_heads].
+ * Alignment: q, pools and o_part 16-byte aligned; the rest 4-byte aligned;
+ * workspace 256-byte aligned.
+ */
+int kf_partial_attn(const kf_shape* shape, const void* q, const void* k_pool,
+                    const void* v_pool, const float* k_scale, const float* v_scale,
+                    const kf_route* routes, int32_t num_routes,
+                    int32_t max_pages_per_route, const int32_t* page_ids,
+                    float* o_part, float* lse_part, void* workspace,
+                    size_t workspace_bytes, int32_t* err_flags, void* stream);
+
+/*
+ * kf_merge_partials -- log-sum-exp merge of the partials of each sequence
+ * (Section 3.2, step 4): over the routes r of sequence b,
+ *   M = max_r lse_r,  w_r = exp(lse_r - M),
+ *   out[b][h][:] = sum_r w_r o_part[r][h][:] / sum_r w_r,
+ *   lse_out[b][h] = M + ln sum_r w_r.
+ * A sequence with no routes, or only empty ones, gives out = 0, lse = -inf.
+ * A CSR row outside [0, num_routes] or decreasing gives NaN +
+ * KF_EFLAG_BAD_ROUTE.  out [num_seqs][num_q_heads][head_dim] float32,
+ * lse_out [num_seqs][num_q_heads]; head_dim must be KF_HEAD_DIM.
+ * Alignment: o_part and out 8-byte aligned; the rest 4-byte aligned.
+ */
+int kf_merge_partials(int32_t num_seqs, int32_t num_routes, int32_t num_q_heads,
+                      int32_t head_dim, const float* o_part, const float* lse_part,
+                      const int32_t* seq_route_begin, float* out, float* lse_out,
+                      int32_t* err_flags, void* stream);
+
+/* Static description of a status code (never NULL). */
+const char* kf_status_str(int status);
+
+/* Library build string, e.g. "kf 0.1 gfx950". */
+const char* kf_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KF_H */

@@ -1,0 +1,189 @@
+// C-ABI layer of libkf: host-side argument checks, workspace sizing and
+// kernel launches on the caller's stream.  Declarations and the contract of
+// every entry point are in include/kf.h.
+#include <math.h>
+#include <stdint.h>
+
+#include "kf.h"
+#include "kf_internal.h"
+
+namespace {
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Checks shared by append and partial attention.
+int check_shape(const kf_shape* s) {
+  if (!s) return KF_ERR_INVALID_ARG;
+  if (s->num_seqs < 0 || s->num_q_heads <= 0 || s->num_kv_heads <= 0 || s->num_pages < 1 ||
+      s->num_page_ids < 0)
+    return KF_ERR_INVALID_ARG;
+  if (s->num_q_heads % s->num_kv_heads != 0) return KF_ERR_INVALID_ARG;
+  if (s->num_q_heads / s->num_kv_heads > KF_MAX_GROUP) return KF_ERR_UNSUPPORTED;
+  if (s->head_dim != KF_HEAD_DIM || s->page_size != KF_PAGE_SIZE) return KF_ERR_UNSUPPORTED;
+  if (s->kv_dtype != KF_KV_BF16 && s->kv_dtype != KF_KV_FP8_E4M3) return KF_ERR_UNSUPPORTED;
+  if (!isfinite(s->scale)) return KF_ERR_INVALID_ARG;
+  // element offsets of the pools are formed in 64 bits; the grid needs
+  // num_kv_heads <= 65535 (checked per call together with num_routes)
+  return KF_OK;
+}
+
+hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+}  // namespace
+
+namespace kf {
+
+WorkspaceLayout workspace_layout(int32_t num_routes, int32_t num_kv_heads, int32_t group,
+                                 int32_t max_chunks) {
+  WorkspaceLayout l;
+  const size_t units = (size_t)num_routes * num_kv_heads;
+  const size_t recs = units * (size_t)max_chunks * (size_t)group;
+  l.counters_off = 0;
+  l.ml_off = round_up(units * sizeof(int32_t), 256);
+  l.o_off = l.ml_off + round_up(recs * 2 * sizeof(float), 256);
+  l.total = l.o_off + round_up(recs * kDim * sizeof(float), 256);
+  return l;
+}
+
+}  // namespace kf
+
+extern "C" {
+
+const char* kf_status_str(int status) {
+  switch (status) {
+    case KF_OK: return "ok";
+    case KF_ERR_INVALID_ARG: return "invalid argument";
+    case KF_ERR_UNSUPPORTED: return "unsupported shape or dtype";
+    case KF_ERR_WORKSPACE: return "workspace missing or too small";
+    case KF_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* kf_version(void) { return "kf 0.1 gfx950"; }
+
+int kf_kv_append(const kf_shape* shape, void* k_pool, void* v_pool, const void* k_new,
+                 const void* v_new, kf_route* routes, int32_t num_routes,
+                 const int32_t* tail_route, const int32_t* page_ids, int32_t* err_flags,
+                 void* stream) {
+  int st = check_shape(shape);
+  if (st != KF_OK) return st;
+  if (shape->kv_dtype != KF_KV_BF16) return KF_ERR_UNSUPPORTED;
+  if (num_routes < 0) return KF_ERR_INVALID_ARG;
+  if (shape->num_seqs == 0) return KF_OK;
+  if (!k_pool || !v_pool || !k_new || !v_new || !tail_route || !err_flags ||
+      (num_routes > 0 && !routes) || (shape->num_page_ids > 0 && !page_ids))
+    return KF_ERR_INVALID_ARG;
+  const void* ptrs[] = {k_pool, v_pool, k_new, v_new, routes, tail_route, page_ids, err_flags};
+  for (const void* p : ptrs)
+    if (p && !aligned(p, 4)) return KF_ERR_INVALID_ARG;
+  kf::AppendArgs a;
+  a.k_pool = k_pool;
+  a.v_pool = v_pool;
+  a.k_new = static_cast<const uint16_t*>(k_new);
+  a.v_new = static_cast<const uint16_t*>(v_new);
+  a.routes = routes;
+  a.tail_route = tail_route;
+  a.page_ids = page_ids;
+  a.err_flags = err_flags;
+  a.num_seqs = shape->num_seqs;
+  a.num_kv_heads = shape->num_kv_heads;
+  a.num_routes = num_routes;
+  a.num_pages = shape->num_pages;
+  a.num_page_ids = shape->num_page_ids;
+  return kf::launch_append(a, as_stream(stream)) == hipSuccess ? KF_OK : KF_ERR_HIP;
+}
+
+size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes,
+                                       int32_t max_pages_per_route) {
+  if (check_shape(shape) != KF_OK || num_routes < 0 || max_pages_per_route < 0) return 0;
+  const int32_t group = shape->num_q_heads / shape->num_kv_heads;
+  return kf::workspace_layout(num_routes, shape->num_kv_heads, group,
+                              kf::max_chunks_for(max_pages_per_route))
+      .total;
+}
+
+int kf_partial_attn(const kf_shape* shape, const void* q, const void* k_pool, const void* v_pool,
+                    const float* k_scale, const float* v_scale, const kf_route* routes,
+                    int32_t num_routes, int32_t max_pages_per_route, const int32_t* page_ids,
+                    float* o_part, float* lse_part, void* workspace, size_t workspace_bytes,
+                    int32_t* err_flags, void* stream) {
+  int st = check_shape(shape);
+  if (st != KF_OK) return st;
+  if (num_routes < 0 || max_pages_per_route < 0) return KF_ERR_INVALID_ARG;
+  if (num_routes == 0) return KF_OK;
+  if (num_routes > 65535 || shape->num_kv_heads > 65535) return KF_ERR_UNSUPPORTED;
+  const bool fp8 = shape->kv_dtype == KF_KV_FP8_E4M3;
+  if (!q || !k_pool || !v_pool || !routes || !o_part || !lse_part || !err_flags ||
+      (shape->num_page_ids > 0 && !page_ids))
+    return KF_ERR_INVALID_ARG;
+  if (fp8 && (!k_scale || !v_scale)) return KF_ERR_INVALID_ARG;
+  if (!aligned(q, 16) || !aligned(k_pool, 16) || !aligned(v_pool, 16) || !aligned(o_part, 16))
+    return KF_ERR_INVALID_ARG;
+  const void* p4[] = {k_scale, v_scale, routes, page_ids, lse_part, err_flags};
+  for (const void* p : p4)
+    if (p && !aligned(p, 4)) return KF_ERR_INVALID_ARG;
+  const int32_t group = shape->num_q_heads / shape->num_kv_heads;
+  const int32_t max_chunks = kf::max_chunks_for(max_pages_per_route);
+  const kf::WorkspaceLayout l =
+      kf::workspace_layout(num_routes, shape->num_kv_heads, group, max_chunks);
+  if (!workspace || !aligned(workspace, 256) || workspace_bytes < l.total) return KF_ERR_WORKSPACE;
+
+  kf::PartialArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k_pool = k_pool;
+  a.v_pool = v_pool;
+  a.k_scale = k_scale;
+  a.v_scale = v_scale;
+  a.routes = routes;
+  a.page_ids = page_ids;
+  a.o_part = o_part;
+  a.lse_part = lse_part;
+  char* ws = static_cast<char*>(workspace);
+  a.counters = reinterpret_cast<int32_t*>(ws + l.counters_off);
+  a.ws_ml = reinterpret_cast<float*>(ws + l.ml_off);
+  a.ws_o = reinterpret_cast<float*>(ws + l.o_off);
+  a.err_flags = err_flags;
+  a.num_seqs = shape->num_seqs;
+  a.num_q_heads = shape->num_q_heads;
+  a.num_kv_heads = shape->num_kv_heads;
+  a.group = group;
+  a.num_routes = num_routes;
+  a.max_pages_per_route = max_pages_per_route;
+  a.max_chunks = max_chunks;
+  a.num_pages = shape->num_pages;
+  a.num_page_ids = shape->num_page_ids;
+  a.scale_log2 = (float)((double)shape->scale * 1.4426950408889634074);
+  return kf::launch_partial(a, fp8, as_stream(stream)) == hipSuccess ? KF_OK : KF_ERR_HIP;
+}
+
+int kf_merge_partials(int32_t num_seqs, int32_t num_routes, int32_t num_q_heads, int32_t head_dim,
+                      const float* o_part, const float* lse_part, const int32_t* seq_route_begin,
+                      float* out, float* lse_out, int32_t* err_flags, void* stream) {
+  if (num_seqs < 0 || num_routes < 0 || num_q_heads <= 0) return KF_ERR_INVALID_ARG;
+  if (head_dim != KF_HEAD_DIM) return KF_ERR_UNSUPPORTED;
+  if (num_seqs == 0) return KF_OK;
+  if (num_seqs > 65535 || num_q_heads > 65535) return KF_ERR_UNSUPPORTED;
+  if (!seq_route_begin || !out || !lse_out || !err_flags ||
+      (num_routes > 0 && (!o_part || !lse_part)))
+    return KF_ERR_INVALID_ARG;
+  if ((o_part && !aligned(o_part, 8)) || !aligned(out, 8)) return KF_ERR_INVALID_ARG;
+  const void* p4[] = {lse_part, seq_route_begin, lse_out, err_flags};
+  for (const void* p : p4)
+    if (p && !aligned(p, 4)) return KF_ERR_INVALID_ARG;
+  kf::MergeArgs a;
+  a.o_part = o_part;
+  a.lse_part = lse_part;
+  a.seq_route_begin = seq_route_begin;
+  a.out = out;
+  a.lse_out = lse_out;
+  a.err_flags = err_flags;
+  a.num_seqs = num_seqs;
+  a.num_routes = num_routes;
+  a.num_q_heads = num_q_heads;
+  return kf::launch_merge(a, as_stream(stream)) == hipSuccess ? KF_OK : KF_ERR_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,475 @@
+// gfx950 kernels of the weightless attention node's decode step
+// (KernelFlume, arXiv 2606.29207, Section 3.2 steps 3-4, Section 5.1):
+//   append_kernel   -- tail append of the step's K/V token
+//   partial_kernel  -- local attention over token-range routes -> (o, lse)
+//   merge_kernel    -- log-sum-exp merge of the partials of each sequence
+//
+// partial_kernel is HBM-bound (4 flop per KV byte at 4 query heads per KV
+// head).  One 256-thread workgroup owns (route, KV head, chunk of <= 64
+// pages); each of its four waves streams 4-page tiles:
+//   * lane (grp = lane/16, i = lane%16).  For q.K^T the MFMA A operand row i
+//     is token (page i/4 of the tile, slot 4c + i%4) for c = 0..3, so the
+//     16x16 result lands with lane (grp, head i) holding all 16 scores of
+//     page grp of the tile.  Those are exactly the P^T values the same lane
+//     feeds as the B operand of p.V, whose A operand is read straight from
+//     the dimension-major V page (V^T rows are contiguous in slots): no LDS
+//     or cross-lane traffic between the two products.
+//   * both products use v_mfma_f32_16x16x32_bf16; query heads of the group
+//     fill the N = 16 columns (G <= 16, the rest zero).
+//   * p (fp32) enters p.V as bf16 hi + bf16 lo, two MFMAs, so the products
+//     carry ~2^-17 relative error instead of bf16's 2^-9.
+//   * softmax state per head is shared by the four lane groups (max reduced
+//     across groups per tile), the running sum is kept per lane and reduced
+//     once at the end.
+// Workgroups of one (route, KV head) write chunk partials to the workspace;
+// the last one to finish (atomic ticket) combines them in chunk order, so
+// results are deterministic and a single kernel produces o_part/lse_part.
+#include "kf_internal.h"
+
+namespace kf {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kLn2 = 0.69314718055994530942f;
+constexpr int kThreads = kWaves * 64;
+constexpr int kTilesPerWave = kChunkPages / kTilePages / kWaves;  // 4
+constexpr int kLdsStride = kDim + 4;  // padded row of the per-wave output buffer
+
+static_assert(kTilesPerWave * kTilePages * kWaves == kChunkPages, "chunk must tile evenly");
+static_assert(kTilesPerWave * kTilePages <= 16, "page ids of a wave must fit 16 lanes");
+
+__device__ __forceinline__ float neg_inf() { return -__builtin_inff(); }
+__device__ __forceinline__ float qnan() { return __builtin_nanf(""); }
+
+__device__ __forceinline__ f32x4 mfma16(u32x4 a, u32x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ uint32_t pack_bf16_rne(float lo, float hi) {
+  bf16x2 v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+// 16 E4M3FN codes (one dword = 4 codes, lowest byte first) -> 16 bf16 in two
+// 8-element operands, exactly (every E4M3 value is a bf16 value).
+__device__ __forceinline__ void fp8x16_to_bf16(u32x4 codes, u32x4& lo8, u32x4& hi8) {
+  uint32_t o[8];
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    o[2 * w] = __builtin_bit_cast(uint32_t,
+                                  __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(codes[w], 1.0f, false));
+    o[2 * w + 1] = __builtin_bit_cast(uint32_t,
+                                      __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(codes[w], 1.0f, true));
+  }
+  lo8 = u32x4{o[0], o[1], o[2], o[3]};
+  hi8 = u32x4{o[4], o[5], o[6], o[7]};
+}
+
+template <class T>
+__device__ __forceinline__ u32x4 ld16(const T* p) {
+  return *reinterpret_cast<const u32x4*>(p);
+}
+
+// ------------------------------------------------------------------- append
+__global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
+  const int b = blockIdx.x;
+  const int r = a.tail_route[b];
+  if (r < 0) return;
+  int flag = 0;
+  int32_t seq = 0, tb = 0, te = 0, base = 0, cap = 0, pid = 0;
+  if (r >= a.num_routes) {
+    flag = KF_EFLAG_BAD_ROUTE;
+  } else {
+    const int32_t* rp = reinterpret_cast<const int32_t*>(a.routes + r);
+    seq = rp[0]; tb = rp[2]; te = rp[3]; base = rp[4]; cap = rp[5];
+    const int j = te - tb;
+    if (seq != b || j < 0) {
+      flag = KF_EFLAG_BAD_ROUTE;
+    } else if (j / kPage >= cap) {
+      flag = KF_EFLAG_TAIL_FULL;
+    } else if (base < 0 || (int64_t)base + j / kPage >= a.num_page_ids) {
+      flag = KF_EFLAG_BAD_ROUTE;
+    } else {
+      pid = a.page_ids[base + j / kPage];
+      if (pid < 0 || pid >= a.num_pages) flag = KF_EFLAG_BAD_PAGE;
+    }
+  }
+  if (flag) {
+    if (threadIdx.x == 0) atomicOr(a.err_flags, flag);
+    return;
+  }
+  const int slot = (te - tb) % kPage;
+  const int H = a.num_kv_heads;
+  uint16_t* kp = static_cast<uint16_t*>(a.k_pool);
+  uint16_t* vp = static_cast<uint16_t*>(a.v_pool);
+  for (int e = threadIdx.x; e < H * kDim; e += blockDim.x) {
+    const int g = e / kDim, d = e % kDim;
+    const size_t head = (size_t)pid * H + g;
+    const uint16_t kv = a.k_new[((size_t)b * H + g) * kDim + d];
+    const uint16_t vv = a.v_new[((size_t)b * H + g) * kDim + d];
+    kp[(head * kPage + slot) * kDim + d] = kv;
+    vp[(head * kDim + d) * kPage + slot] = vv;
+  }
+  __syncthreads();  // every thread has read tok_end before it moves
+  if (threadIdx.x == 0) a.routes[r].tok_end = te + 1;
+}
+
+// ------------------------------------------------------------------ partial
+template <bool FP8>
+__global__ __launch_bounds__(kThreads) void partial_kernel(PartialArgs a) {
+  __shared__ float s_o[kWaves][KF_MAX_GROUP][kLdsStride];
+  __shared__ float s_m[kWaves][KF_MAX_GROUP];
+  __shared__ float s_l[kWaves][KF_MAX_GROUP];
+  __shared__ float s_fm[KF_MAX_GROUP];
+  __shared__ float s_fl[KF_MAX_GROUP];
+  __shared__ int s_last;
+
+  const int c = blockIdx.x, g = blockIdx.y, r = blockIdx.z;
+  const int G = a.group, Hq = a.num_q_heads, H = a.num_kv_heads;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, grp = lane >> 4, li = lane & 15;
+  const int hq0 = g * G;
+
+  const int32_t* rp = reinterpret_cast<const int32_t*>(a.routes + r);
+  const int seq = rp[0], tb = rp[2], te = rp[3], base = rp[4], cap = rp[5];
+  const int n = te - tb;
+  const int npages = n > 0 ? (n + kPage - 1) / kPage : 0;
+  const bool bad = seq < 0 || seq >= a.num_seqs || n < 0 || base < 0 || npages > cap ||
+                   npages > a.max_pages_per_route || (int64_t)base + npages > a.num_page_ids;
+  if (bad || npages == 0) {
+    if (c == 0) {
+      const float ov = bad ? qnan() : 0.0f, lv = bad ? qnan() : neg_inf();
+      for (int e = tid; e < G * kDim; e += kThreads)
+        a.o_part[((size_t)r * Hq + hq0 + e / kDim) * kDim + e % kDim] = ov;
+      if (tid < G) a.lse_part[(size_t)r * Hq + hq0 + tid] = lv;
+      if (bad && tid == 0) atomicOr(a.err_flags, KF_EFLAG_BAD_ROUTE);
+    }
+    return;
+  }
+  const int nchunks = (npages + kChunkPages - 1) / kChunkPages;
+  if (c >= nchunks) return;
+  const int p0 = (int)((int64_t)c * npages / nchunks);
+  const int p1 = (int)((int64_t)(c + 1) * npages / nchunks);
+  const int ntiles = (p1 - p0 + kTilePages - 1) / kTilePages;
+  const int lim = min(n, p1 * kPage);  // route-local token bound of this chunk
+
+  // Page ids of this wave's tiles: lane l < 16 holds page (l % 4) of the
+  // wave's tile number l / 4.  Pages past the chunk read page 0 (masked).
+  int my_pid = 0;
+  bool pid_bad = false;
+  if (lane < kTilesPerWave * kTilePages) {
+    const int tt = w + kWaves * (lane / kTilePages);
+    const int pg = p0 + tt * kTilePages + lane % kTilePages;
+    if (tt < ntiles && pg < p1) {
+      const int v = a.page_ids[base + pg];
+      if (v < 0 || v >= a.num_pages) pid_bad = true;
+      else my_pid = v;
+    }
+  }
+  const bool wave_bad = __ballot(pid_bad) != 0;
+
+  // B operand of q.K^T: query head hq0 + li (zero columns past the group).
+  u32x4 qb[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    const int d0 = FP8 ? 64 * (kk >> 1) + 16 * grp + 8 * (kk & 1) : 32 * kk + 8 * grp;
+    qb[kk] = li < G ? ld16(a.q + ((size_t)seq * Hq + hq0 + li) * kDim + d0) : u32x4{0, 0, 0, 0};
+  }
+
+  const size_t head_elems = (size_t)kPage * kDim;  // elements of one (page, kv head)
+  f32x4 oacc[8];
+#pragma unroll
+  for (int b8 = 0; b8 < 8; ++b8) oacc[b8] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = neg_inf(), l_run = 0.0f;
+
+  for (int k = 0; k < kTilesPerWave; ++k) {
+    const int tt = w + kWaves * k;
+    if (tt >= ntiles) break;
+    const int tp0 = p0 + tt * kTilePages;  // route-local first page of the tile
+    const int pidK = __shfl(my_pid, kTilePages * k + (li >> 2));
+    const int pidV = __shfl(my_pid, kTilePages * k + grp);
+
+    // ---- loads: K rows for q.K^T, V^T rows for p.V
+    u32x4 kr[4][4];  // [c][kk]
+    u32x4 vr[8][2];  // [d block][slot half]
+    if constexpr (!FP8) {
+      const uint16_t* kb = static_cast<const uint16_t*>(a.k_pool) +
+                           ((size_t)pidK * H + g) * head_elems + (li & 3) * kDim + 8 * grp;
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc)
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) kr[cc][kk] = ld16(kb + 4 * cc * kDim + 32 * kk);
+      const uint16_t* vb = static_cast<const uint16_t*>(a.v_pool) +
+                           ((size_t)pidV * H + g) * head_elems + li * kPage;
+#pragma unroll
+      for (int b8 = 0; b8 < 8; ++b8) {
+        vr[b8][0] = ld16(vb + b8 * 16 * kPage);
+        vr[b8][1] = ld16(vb + b8 * 16 * kPage + 8);
+      }
+    } else {
+      const uint8_t* kb = static_cast<const uint8_t*>(a.k_pool) +
+                          ((size_t)pidK * H + g) * head_elems + (li & 3) * kDim + 16 * grp;
+      u32x4 kc[4][2];
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc)
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp) kc[cc][pp] = ld16(kb + 4 * cc * kDim + 64 * pp);
+      const uint8_t* vb = static_cast<const uint8_t*>(a.v_pool) +
+                          ((size_t)pidV * H + g) * head_elems + li * kPage;
+      u32x4 vc[8];
+#pragma unroll
+      for (int b8 = 0; b8 < 8; ++b8) vc[b8] = ld16(vb + b8 * 16 * kPage);
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc)
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp) fp8x16_to_bf16(kc[cc][pp], kr[cc][2 * pp], kr[cc][2 * pp + 1]);
+#pragma unroll
+      for (int b8 = 0; b8 < 8; ++b8) fp8x16_to_bf16(vc[b8], vr[b8][0], vr[b8][1]);
+    }
+
+    // ---- S^T = K Q^T: lane (grp, head li) gets slots 4c + r4 of page grp
+    f32x4 s[4];
+#pragma unroll
+    for (int cc = 0; cc < 4; ++cc) {
+      s[cc] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) s[cc] = mfma16(kr[cc][kk], qb[kk], s[cc]);
+    }
+
+    float ks = a.scale_log2, vs = 1.0f;
+    if constexpr (FP8) {
+      ks *= a.k_scale[(size_t)pidV * H + g];
+      vs = a.v_scale[(size_t)pidV * H + g];
+    }
+    const int tok0 = (tp0 + grp) * kPage;  // route-local token of slot 0 of page grp
+    float mt = neg_inf();
+#pragma unroll
+    for (int cc = 0; cc < 4; ++cc)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const float v = (tok0 + 4 * cc + r4 < lim) ? s[cc][r4] * ks : neg_inf();
+        s[cc][r4] = v;
+        mt = fmaxf(mt, v);
+      }
+    mt = fmaxf(mt, __shfl_xor(mt, 16));
+    mt = fmaxf(mt, __shfl_xor(mt, 32));
+    const float m_new = fmaxf(m_run, mt);
+    const float alpha = exp2_fast(m_run - m_new);
+    m_run = m_new;
+    l_run *= alpha;
+#pragma unroll
+    for (int b8 = 0; b8 < 8; ++b8) oacc[b8] *= alpha;
+
+    // ---- P^T operands: slots 8*h2 .. 8*h2+7 of page grp, as bf16 hi + lo
+    u32x4 phi[2], plo[2];
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int cc = 2 * h2 + (jj >> 1), r4 = 2 * (jj & 1);
+        const float e0 = exp2_fast(s[cc][r4] - m_new);
+        const float e1 = exp2_fast(s[cc][r4 + 1] - m_new);
+        l_run += e0 + e1;
+        const float x0 = e0 * vs, x1 = e1 * vs;
+        const uint32_t b0 = __builtin_bit_cast(uint32_t, x0) & 0xFFFF0000u;
+        const uint32_t b1 = __builtin_bit_cast(uint32_t, x1) & 0xFFFF0000u;
+        phi[h2][jj] = (b0 >> 16) | b1;
+        plo[h2][jj] = pack_bf16_rne(x0 - __builtin_bit_cast(float, b0),
+                                    x1 - __builtin_bit_cast(float, b1));
+      }
+    }
+
+    // ---- zero V of slots past the chunk (unused slots may hold anything)
+    if ((tp0 + kTilePages) * kPage > lim) {
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+        for (int wd = 0; wd < 4; ++wd) {
+          const int t = tok0 + 8 * h2 + 2 * wd;
+          const uint32_t msk = (t < lim ? 0x0000FFFFu : 0u) | (t + 1 < lim ? 0xFFFF0000u : 0u);
+#pragma unroll
+          for (int b8 = 0; b8 < 8; ++b8) vr[b8][h2][wd] &= msk;
+        }
+    }
+
+    // ---- O^T += V^T P^T
+#pragma unroll
+    for (int b8 = 0; b8 < 8; ++b8)
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        oacc[b8] = mfma16(vr[b8][h2], phi[h2], oacc[b8]);
+        oacc[b8] = mfma16(vr[b8][h2], plo[h2], oacc[b8]);
+      }
+  }
+
+  l_run += __shfl_xor(l_run, 16);
+  l_run += __shfl_xor(l_run, 32);
+  if (wave_bad) m_run = qnan();
+
+  // ---- combine the four waves: lane (grp, li) holds d = 16*b8 + 4*grp + r4
+  if (li < G) {
+#pragma unroll
+    for (int b8 = 0; b8 < 8; ++b8)
+      *reinterpret_cast<f32x4*>(&s_o[w][li][16 * b8 + 4 * grp]) = oacc[b8];
+    if (grp == 0) {
+      s_m[w][li] = m_run;
+      s_l[w][li] = l_run;
+    }
+  }
+  __syncthreads();
+  if (tid < G) {
+    float M = neg_inf();
+    for (int ww = 0; ww < kWaves; ++ww) M = fmaxf(M, s_m[ww][tid]);
+    float L = 0.0f;
+    for (int ww = 0; ww < kWaves; ++ww) {
+      const float mw = s_m[ww][tid];
+      const float wt = mw == neg_inf() ? 0.0f : exp2_fast(mw - M);
+      s_m[ww][tid] = wt;  // becomes the wave's weight
+      L += wt * s_l[ww][tid];
+    }
+    s_fm[tid] = M;
+    s_fl[tid] = L;
+  }
+  if (tid == 0 && wave_bad) atomicOr(a.err_flags, KF_EFLAG_BAD_PAGE);
+  __syncthreads();
+  // a wave that met a bad page has m = NaN, so its weight poisons the chunk
+
+  if (nchunks == 1) {
+    for (int e = tid; e < G * kDim; e += kThreads) {
+      const int h = e / kDim, d = e % kDim;
+      float O = 0.0f;
+#pragma unroll
+      for (int ww = 0; ww < kWaves; ++ww) O += s_m[ww][h] * s_o[ww][h][d];
+      a.o_part[((size_t)r * Hq + hq0 + h) * kDim + d] = O / s_fl[h];
+    }
+    if (tid < G)
+      a.lse_part[(size_t)r * Hq + hq0 + tid] = (s_fm[tid] + __log2f(s_fl[tid])) * kLn2;
+    return;
+  }
+
+  const size_t rec0 = ((size_t)r * H + g) * a.max_chunks;
+  {
+    const size_t rec = rec0 + c;
+    for (int e = tid; e < G * kDim; e += kThreads) {
+      const int h = e / kDim, d = e % kDim;
+      float O = 0.0f;
+#pragma unroll
+      for (int ww = 0; ww < kWaves; ++ww) O += s_m[ww][h] * s_o[ww][h][d];
+      a.ws_o[(rec * G + h) * kDim + d] = O;
+    }
+    if (tid < G) {
+      a.ws_ml[(rec * G + tid) * 2] = s_fm[tid];
+      a.ws_ml[(rec * G + tid) * 2 + 1] = s_fl[tid];
+    }
+  }
+  __threadfence();
+  __syncthreads();
+  if (tid == 0) {
+    const int old = atomicAdd(a.counters + (size_t)r * H + g, 1);
+    s_last = old == nchunks - 1;
+  }
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+
+  // ---- last workgroup of (route, kv head): combine chunks 0..nchunks-1
+  if (tid < G) {
+    float M = neg_inf();
+    for (int cc = 0; cc < nchunks; ++cc) M = fmaxf(M, a.ws_ml[((rec0 + cc) * G + tid) * 2]);
+    float L = 0.0f;
+    for (int cc = 0; cc < nchunks; ++cc) {
+      const float mc = a.ws_ml[((rec0 + cc) * G + tid) * 2];
+      L += exp2_fast(mc - M) * a.ws_ml[((rec0 + cc) * G + tid) * 2 + 1];
+    }
+    s_fm[tid] = M;
+    s_fl[tid] = L;
+  }
+  __syncthreads();
+  for (int e = tid; e < G * kDim; e += kThreads) {
+    const int h = e / kDim, d = e % kDim;
+    const float M = s_fm[h];
+    float O = 0.0f;
+    for (int cc = 0; cc < nchunks; ++cc) {
+      const float mc = a.ws_ml[((rec0 + cc) * G + h) * 2];
+      O += exp2_fast(mc - M) * a.ws_o[((rec0 + cc) * G + h) * kDim + d];
+    }
+    a.o_part[((size_t)r * Hq + hq0 + h) * kDim + d] = O / s_fl[h];
+  }
+  if (tid < G)
+    a.lse_part[(size_t)r * Hq + hq0 + tid] = (s_fm[tid] + __log2f(s_fl[tid])) * kLn2;
+  if (tid == 0) a.counters[(size_t)r * H + g] = 0;
+}
+
+// -------------------------------------------------------------------- merge
+// One wave per (query head, sequence); lane holds dims 2*lane, 2*lane+1.
+__global__ __launch_bounds__(64) void merge_kernel(MergeArgs a) {
+  const int h = blockIdx.x, b = blockIdx.y, lane = threadIdx.x;
+  const int Hq = a.num_q_heads;
+  const int r0 = a.seq_route_begin[b], r1 = a.seq_route_begin[b + 1];
+  float2* out = reinterpret_cast<float2*>(a.out + ((size_t)b * Hq + h) * kDim) + lane;
+  float* lse_out = a.lse_out + (size_t)b * Hq + h;
+  if (r0 < 0 || r1 < r0 || r1 > a.num_routes) {
+    *out = make_float2(qnan(), qnan());
+    if (lane == 0) {
+      *lse_out = qnan();
+      if (h == 0) atomicOr(a.err_flags, KF_EFLAG_BAD_ROUTE);
+    }
+    return;
+  }
+  constexpr float kLog2e = 1.44269504088896340736f;
+  float M = neg_inf();
+  bool any_nan = false;
+  for (int r = r0; r < r1; ++r) {
+    const float l = a.lse_part[(size_t)r * Hq + h];
+    any_nan |= l != l;
+    M = fmaxf(M, l);
+  }
+  if (any_nan || M == neg_inf()) {
+    const float v = any_nan ? qnan() : 0.0f;
+    *out = make_float2(v, v);
+    if (lane == 0) *lse_out = any_nan ? qnan() : neg_inf();
+    return;
+  }
+  float L = 0.0f, o0 = 0.0f, o1 = 0.0f;
+  for (int r = r0; r < r1; ++r) {
+    const float wr = exp2_fast((a.lse_part[(size_t)r * Hq + h] - M) * kLog2e);
+    const float2 v = reinterpret_cast<const float2*>(a.o_part + ((size_t)r * Hq + h) * kDim)[lane];
+    L += wr;
+    o0 += wr * v.x;
+    o1 += wr * v.y;
+  }
+  *out = make_float2(o0 / L, o1 / L);
+  if (lane == 0) *lse_out = M + __logf(L);
+}
+
+}  // namespace
+
+hipError_t launch_append(const AppendArgs& a, hipStream_t stream) {
+  if (a.num_seqs == 0) return hipSuccess;
+  hipLaunchKernelGGL(append_kernel, dim3(a.num_seqs), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_partial(const PartialArgs& a, bool fp8, hipStream_t stream) {
+  if (a.num_routes == 0) return hipSuccess;
+  const dim3 grid(a.max_chunks, a.num_kv_heads, a.num_routes);
+  if (fp8)
+    hipLaunchKernelGGL(partial_kernel<true>, grid, dim3(kThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL(partial_kernel<false>, grid, dim3(kThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_merge(const MergeArgs& a, hipStream_t stream) {
+  if (a.num_seqs == 0 || a.num_q_heads == 0) return hipSuccess;
+  hipLaunchKernelGGL(merge_kernel, dim3(a.num_q_heads, a.num_seqs), dim3(64), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace kf

@@ -1,0 +1,226 @@
+"""Thin ctypes binding of libkf.so (include/kf.h) for torch device tensors.
+
+Argument marshalling only: every step runs in the library's HIP kernels on
+the current torch stream.  Importing works without a GPU; calling an entry
+point without the built library raises ``KFError``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkf.so")
+
+PAGE_SIZE = 16
+HEAD_DIM = 128
+MAX_GROUP = 16
+
+KV_BF16 = 0
+KV_FP8_E4M3 = 1
+
+EFLAG_TAIL_FULL = 1
+EFLAG_BAD_ROUTE = 2
+EFLAG_BAD_PAGE = 4
+
+# every symbol include/kf.h declares
+EXPORTS = ("kf_kv_append", "kf_partial_attn_workspace_bytes", "kf_partial_attn",
+           "kf_merge_partials", "kf_status_str", "kf_version")
+
+
+class KFError(RuntimeError):
+    pass
+
+
+class Route(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("seq", "part", "tok_begin", "tok_end", "page_base", "page_cap")]
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [("num_seqs", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("page_size", ctypes.c_int32), ("kv_dtype", ctypes.c_int32),
+                ("num_pages", ctypes.c_int32), ("num_page_ids", ctypes.c_int32),
+                ("scale", ctypes.c_float)]
+
+
+_lib = None
+
+
+def load(path: str | None = None) -> ctypes.CDLL:
+    """Load libkf.so once; raise if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = path or _LIB_PATH
+    if not os.path.exists(path):
+        raise KFError(f"{path} is missing: build it with `python -m paper_2606_29207_amd.build`")
+    lib = ctypes.CDLL(path)
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    sp = ctypes.POINTER(Shape)
+    lib.kf_kv_append.argtypes = [sp, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp]
+    lib.kf_kv_append.restype = ctypes.c_int
+    lib.kf_partial_attn_workspace_bytes.argtypes = [sp, i32, i32]
+    lib.kf_partial_attn_workspace_bytes.restype = sz
+    lib.kf_partial_attn.argtypes = [sp, vp, vp, vp, vp, vp, vp, i32, i32, vp, vp, vp, vp, sz, vp, vp]
+    lib.kf_partial_attn.restype = ctypes.c_int
+    lib.kf_merge_partials.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]
+    lib.kf_merge_partials.restype = ctypes.c_int
+    lib.kf_status_str.argtypes = [ctypes.c_int]
+    lib.kf_status_str.restype = ctypes.c_char_p
+    lib.kf_version.argtypes = []
+    lib.kf_version.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def status_str(status: int) -> str:
+    return load().kf_status_str(status).decode()
+
+
+def version() -> str:
+    return load().kf_version().decode()
+
+
+def _check(status: int, what: str):
+    if status != 0:
+        raise KFError(f"{what}: {status_str(status)} ({status})")
+
+
+def _ptr(t: torch.Tensor | None):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dev(t: torch.Tensor, name: str, dtype=None):
+    if not t.is_cuda:
+        raise KFError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise KFError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype not in (dtype if isinstance(dtype, tuple) else (dtype,)):
+        raise KFError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    return t
+
+
+def _need(cond, msg):
+    if not cond:
+        raise KFError(msg)
+
+
+def _check_tables(shape: Shape, k_pool, v_pool, routes, page_ids):
+    """Sizes the C ABI cannot see: pools, route rows and page ids."""
+    P, H = shape.num_pages, shape.num_kv_heads
+    esz = 1 if shape.kv_dtype == KV_FP8_E4M3 else 2
+    for t, n in ((k_pool, "k_pool"), (v_pool, "v_pool")):
+        _need(t.element_size() == esz and t.numel() == P * H * PAGE_SIZE * HEAD_DIM,
+              f"{n} must hold [num_pages, num_kv_heads, 16, 128] elements of the pool dtype")
+    _need(routes.dtype == torch.int32 and routes.dim() == 2 and routes.shape[1] == 6,
+          "routes must be int32 [R, 6]")
+    _need(page_ids.dtype == torch.int32 and page_ids.numel() == shape.num_page_ids,
+          "page_ids must be int32 [num_page_ids]")
+    _need(shape.num_seqs >= 0, "bad shape")
+
+
+def make_shape(num_seqs, num_q_heads, num_kv_heads, kv_dtype, num_pages, num_page_ids,
+               scale) -> Shape:
+    return Shape(num_seqs, num_q_heads, num_kv_heads, HEAD_DIM, PAGE_SIZE, kv_dtype,
+                 num_pages, num_page_ids, float(scale))
+
+
+def _pool_dtype(k_pool: torch.Tensor) -> int:
+    return KV_FP8_E4M3 if k_pool.element_size() == 1 else KV_BF16
+
+
+def shape_of(q, k_pool, page_ids, scale) -> Shape:
+    """kf_shape from q [B, Hq, 128], K pool [P, Hkv, 16, 128] and page_ids."""
+    return make_shape(q.shape[0], q.shape[1], k_pool.shape[1], _pool_dtype(k_pool),
+                      k_pool.shape[0], page_ids.numel(), scale)
+
+
+def kv_append(shape: Shape, k_pool, v_pool, k_new, v_new, routes, tail_route, page_ids,
+              err_flags, stream=None):
+    """kf_kv_append.  routes: int32 [R, 6] (updated in place)."""
+    lib = load()
+    for t, n in ((k_pool, "k_pool"), (v_pool, "v_pool"), (k_new, "k_new"), (v_new, "v_new"),
+                 (routes, "routes"), (tail_route, "tail_route"), (page_ids, "page_ids"),
+                 (err_flags, "err_flags")):
+        _dev(t, n)
+    B, H = shape.num_seqs, shape.num_kv_heads
+    _need(tuple(k_new.shape) == (B, H, HEAD_DIM) and tuple(v_new.shape) == (B, H, HEAD_DIM),
+          "k_new/v_new must be [num_seqs, num_kv_heads, 128]")
+    _need(k_new.element_size() == 2 and v_new.element_size() == 2, "k_new/v_new must be bf16")
+    _need(tail_route.numel() >= B and tail_route.dtype == torch.int32, "tail_route: int32 [num_seqs]")
+    _check_tables(shape, k_pool, v_pool, routes, page_ids)
+    st = lib.kf_kv_append(ctypes.byref(shape), _ptr(k_pool), _ptr(v_pool), _ptr(k_new),
+                          _ptr(v_new), _ptr(routes), routes.shape[0], _ptr(tail_route),
+                          _ptr(page_ids), _ptr(err_flags), _stream(stream))
+    _check(st, "kf_kv_append")
+
+
+def partial_attn_workspace_bytes(shape: Shape, num_routes: int, max_pages_per_route: int) -> int:
+    return int(load().kf_partial_attn_workspace_bytes(ctypes.byref(shape), num_routes,
+                                                       max_pages_per_route))
+
+
+def alloc_workspace(shape: Shape, num_routes: int, max_pages_per_route: int, device="cuda"):
+    n = partial_attn_workspace_bytes(shape, num_routes, max_pages_per_route)
+    if n == 0:
+        raise KFError("invalid workspace request")
+    return torch.zeros(n, dtype=torch.uint8, device=device)
+
+
+def partial_attn(shape: Shape, q, k_pool, v_pool, routes, max_pages_per_route, page_ids,
+                 o_part, lse_part, workspace, err_flags, k_scale=None, v_scale=None,
+                 stream=None):
+    """kf_partial_attn.  o_part float32 [R, Hq, 128], lse_part float32 [R, Hq]."""
+    lib = load()
+    for t, n in ((q, "q"), (k_pool, "k_pool"), (v_pool, "v_pool"), (routes, "routes"),
+                 (page_ids, "page_ids"), (o_part, "o_part"), (lse_part, "lse_part"),
+                 (workspace, "workspace"), (err_flags, "err_flags")):
+        _dev(t, n)
+    if o_part.dtype != torch.float32 or lse_part.dtype != torch.float32:
+        raise KFError("o_part and lse_part must be float32")
+    R = routes.shape[0]
+    _need(tuple(q.shape) == (shape.num_seqs, shape.num_q_heads, HEAD_DIM) and q.element_size() == 2,
+          "q must be bf16 [num_seqs, num_q_heads, 128]")
+    _need(tuple(o_part.shape) == (R, shape.num_q_heads, HEAD_DIM), "o_part must be [R, Hq, 128]")
+    _need(tuple(lse_part.shape) == (R, shape.num_q_heads), "lse_part must be [R, Hq]")
+    _check_tables(shape, k_pool, v_pool, routes, page_ids)
+    if shape.kv_dtype == KV_FP8_E4M3:
+        for t, n in ((k_scale, "k_scale"), (v_scale, "v_scale")):
+            _need(t is not None, f"{n} is required for fp8 pools")
+            _dev(t, n)
+            _need(t.dtype == torch.float32 and t.numel() >= shape.num_pages * shape.num_kv_heads,
+                  f"{n} must be float32 [num_pages, num_kv_heads]")
+    st = lib.kf_partial_attn(ctypes.byref(shape), _ptr(q), _ptr(k_pool), _ptr(v_pool),
+                             _ptr(k_scale), _ptr(v_scale), _ptr(routes), routes.shape[0],
+                             int(max_pages_per_route), _ptr(page_ids), _ptr(o_part),
+                             _ptr(lse_part), _ptr(workspace), workspace.numel(),
+                             _ptr(err_flags), _stream(stream))
+    _check(st, "kf_partial_attn")
+
+
+def merge_partials(num_seqs, o_part, lse_part, seq_route_begin, out, lse_out, err_flags,
+                   stream=None):
+    """kf_merge_partials.  out float32 [B, Hq, 128], lse_out float32 [B, Hq]."""
+    lib = load()
+    for t, n in ((o_part, "o_part"), (lse_part, "lse_part"), (seq_route_begin, "seq_route_begin"),
+                 (out, "out"), (lse_out, "lse_out"), (err_flags, "err_flags")):
+        _dev(t, n)
+    R, Hq, D = o_part.shape
+    _need(o_part.dtype == torch.float32 and lse_part.dtype == torch.float32, "partials must be float32")
+    _need(tuple(lse_part.shape) == (R, Hq), "lse_part must be [R, Hq]")
+    _need(seq_route_begin.dtype == torch.int32 and seq_route_begin.numel() >= num_seqs + 1,
+          "seq_route_begin must be int32 [num_seqs + 1]")
+    _need(tuple(out.shape) == (num_seqs, Hq, D) and out.dtype == torch.float32, "out must be float32 [B, Hq, D]")
+    _need(tuple(lse_out.shape) == (num_seqs, Hq) and lse_out.dtype == torch.float32, "lse_out must be float32 [B, Hq]")
+    st = lib.kf_merge_partials(int(num_seqs), R, Hq, D, _ptr(o_part), _ptr(lse_part),
+                               _ptr(seq_route_begin), _ptr(out), _ptr(lse_out),
+                               _ptr(err_flags), _stream(stream))
+    _check(st, "kf_merge_partials")

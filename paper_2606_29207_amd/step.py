@@ -1,0 +1,95 @@
+"""Device-resident decode state of one attention layer on one GPU.
+
+Holds the query batch, the paged K/V pools, the routing table (token-range
+routes and page ids) and the output buffers as torch device tensors, and runs
+one decode step as the paper orders it (Section 3.2, steps 3-4; Section 5.1):
+the tail routes append the step's K/V token, every route computes its partial,
+and the partials of each sequence are merged.  Marshalling only: the three
+calls are the library's HIP kernels, enqueued on the current stream.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import kf
+
+
+def _to_dev(a: np.ndarray, device) -> torch.Tensor:
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        t = torch.from_numpy(a.view(np.int16)).view(torch.bfloat16)
+    else:
+        t = torch.from_numpy(a)
+    return t.to(device, non_blocking=False)
+
+
+class DecodeState:
+    """Buffers for one layer's decode step.
+
+    Arrays follow include/kf.h: q uint16 (bf16 bits) [B, Hq, 128]; pools
+    uint16 or uint8 (E4M3 codes) [P, Hkv, 16, 128] / [P, Hkv, 128, 16];
+    scales float32 [P, Hkv] or None; routes int32 [R, 6]; page_ids int32;
+    seq_route_begin int32 [B+1]; tail_route int32 [B].
+    """
+
+    def __init__(self, *, q, k_pool, v_pool, routes, page_ids, seq_route_begin, tail_route,
+                 scale, max_pages_per_route, k_scale=None, v_scale=None, device="cuda"):
+        self.device = torch.device(device)
+        self.q = _to_dev(q, device)
+        self.k_pool = _to_dev(k_pool, device)
+        self.v_pool = _to_dev(v_pool, device)
+        self.k_scale = None if k_scale is None else _to_dev(np.asarray(k_scale, np.float32), device)
+        self.v_scale = None if v_scale is None else _to_dev(np.asarray(v_scale, np.float32), device)
+        self.routes = _to_dev(np.asarray(routes, np.int32).reshape(-1, 6), device)
+        self.page_ids = _to_dev(np.asarray(page_ids, np.int32), device)
+        self.seq_route_begin = _to_dev(np.asarray(seq_route_begin, np.int32), device)
+        self.tail_route = _to_dev(np.asarray(tail_route, np.int32), device)
+        self.max_pages_per_route = int(max_pages_per_route)
+        B, Hq, D = self.q.shape
+        R = self.routes.shape[0]
+        self.num_seqs = B
+        self.shape = kf.shape_of(self.q, self.k_pool, self.page_ids, scale)
+        self.workspace = kf.alloc_workspace(self.shape, R, self.max_pages_per_route, device)
+        self.o_part = torch.empty((R, Hq, D), dtype=torch.float32, device=device)
+        self.lse_part = torch.empty((R, Hq), dtype=torch.float32, device=device)
+        self.out = torch.empty((B, Hq, D), dtype=torch.float32, device=device)
+        self.lse = torch.empty((B, Hq), dtype=torch.float32, device=device)
+        self.err_flags = torch.zeros(1, dtype=torch.int32, device=device)
+
+    @classmethod
+    def from_instance(cls, inst, device="cuda"):
+        """Upload a kf_workloads.Instance (duck-typed)."""
+        return cls(q=inst.q, k_pool=inst.k_pool, v_pool=inst.v_pool, routes=inst.routes,
+                   page_ids=inst.page_ids, seq_route_begin=inst.seq_route_begin,
+                   tail_route=inst.tail_route, scale=inst.scale,
+                   max_pages_per_route=inst.max_pages_per_route,
+                   k_scale=inst.k_scale, v_scale=inst.v_scale, device=device)
+
+    def upload_new_tokens(self, k_new: np.ndarray, v_new: np.ndarray):
+        return _to_dev(k_new, self.device), _to_dev(v_new, self.device)
+
+    # ---------------------------------------------------------------- calls
+    def append(self, k_new: torch.Tensor, v_new: torch.Tensor, stream=None):
+        kf.kv_append(self.shape, self.k_pool, self.v_pool, k_new, v_new, self.routes,
+                     self.tail_route, self.page_ids, self.err_flags, stream)
+
+    def partial(self, stream=None):
+        kf.partial_attn(self.shape, self.q, self.k_pool, self.v_pool, self.routes,
+                        self.max_pages_per_route, self.page_ids, self.o_part, self.lse_part,
+                        self.workspace, self.err_flags, self.k_scale, self.v_scale, stream)
+
+    def merge(self, stream=None):
+        kf.merge_partials(self.num_seqs, self.o_part, self.lse_part, self.seq_route_begin,
+                          self.out, self.lse, self.err_flags, stream)
+
+    def step(self, k_new: torch.Tensor | None = None, v_new: torch.Tensor | None = None,
+             stream=None):
+        """One decode step: append (if new tokens are given) -> partial -> merge."""
+        if k_new is not None:
+            self.append(k_new, v_new, stream)
+        self.partial(stream)
+        self.merge(stream)
+
+    def flags(self) -> int:
+        return int(self.err_flags.item())

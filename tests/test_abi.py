@@ -1,0 +1,136 @@
+"""C-ABI checks that need no GPU: libkf.so loads, exports every function
+include/kf.h declares, and rejects bad arguments on the host before it
+launches anything (each call below carries at least one error)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_29207_amd import kf
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kf.h")
+
+FAKE = 0x10000      # non-null, 256-byte aligned stand-in; never dereferenced here
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(kf._LIB_PATH):
+        from paper_2606_29207_amd import build
+        build.build()
+    return kf.load()
+
+
+def _declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(kf_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_header_and_binding_agree():
+    assert _declared_functions() == sorted(kf.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+    assert kf.version().startswith("kf ")
+
+
+def test_struct_layouts_match_header():
+    assert ctypes.sizeof(kf.Route) == 24
+    assert ctypes.sizeof(kf.Shape) == 36
+
+
+def test_status_strings(lib):
+    for code, text in ((0, "ok"), (-1, "invalid argument"), (-2, "unsupported"),
+                       (-3, "workspace"), (-4, "HIP")):
+        assert text in kf.status_str(code)
+    assert kf.status_str(12345) == "unknown status"
+
+
+def _shape(**kw):
+    d = dict(num_seqs=2, num_q_heads=8, num_kv_heads=2, kv_dtype=kf.KV_BF16, num_pages=10,
+             num_page_ids=10, scale=0.088)
+    d.update(kw)
+    s = kf.make_shape(d["num_seqs"], d["num_q_heads"], d["num_kv_heads"], d["kv_dtype"],
+                      d["num_pages"], d["num_page_ids"], d["scale"])
+    for k in ("head_dim", "page_size"):
+        if k in kw:
+            setattr(s, k, kw[k])
+    return s
+
+
+def _partial(lib, shape, **kw):
+    p = dict(q=FAKE, k=FAKE, v=FAKE, ks=None, vs=None, routes=FAKE, R=4, maxp=8, pids=FAKE,
+             o=FAKE, lse=FAKE, ws=FAKE, wsb=1 << 30, flags=FAKE)
+    p.update(kw)
+    v = lambda x: None if x is None else ctypes.c_void_p(x)  # noqa: E731
+    return lib.kf_partial_attn(ctypes.byref(shape), v(p["q"]), v(p["k"]), v(p["v"]), v(p["ks"]),
+                               v(p["vs"]), v(p["routes"]), p["R"], p["maxp"], v(p["pids"]),
+                               v(p["o"]), v(p["lse"]), v(p["ws"]), p["wsb"], v(p["flags"]), None)
+
+
+@pytest.mark.parametrize("shape_kw,call_kw,status", [
+    ({}, dict(q=None), -1),
+    ({}, dict(o=None), -1),
+    ({}, dict(q=FAKE + 2), -1),                       # misaligned
+    ({}, dict(ws=None), -3),
+    ({}, dict(wsb=16), -3),
+    ({}, dict(ws=FAKE + 64), -3),                    # workspace not 256-byte aligned
+    ({"head_dim": 64}, {}, -2),
+    ({"page_size": 32}, {}, -2),
+    ({"num_q_heads": 7}, {}, -1),                    # not a multiple of Hkv
+    ({"num_q_heads": 34, "num_kv_heads": 2}, {}, -2),  # group 17 > 16
+    ({"kv_dtype": 1}, {}, -1),                       # fp8 without scales
+    ({"kv_dtype": 5}, {}, -2),
+    ({"num_pages": 0}, {}, -1),
+    ({"scale": float("nan")}, {}, -1),
+    ({}, dict(R=-1), -1),
+    ({}, dict(R=70000), -2),
+])
+def test_partial_attn_host_checks(lib, shape_kw, call_kw, status):
+    assert _partial(lib, _shape(**shape_kw), **call_kw) == status
+
+
+def test_partial_attn_zero_routes_is_a_no_op(lib):
+    assert _partial(lib, _shape(), R=0) == 0
+
+
+def test_append_host_checks(lib):
+    v = ctypes.c_void_p
+    s = _shape(kv_dtype=kf.KV_FP8_E4M3)
+    args = [v(FAKE)] * 4 + [v(FAKE), 4, v(FAKE), v(FAKE), v(FAKE), None]
+    assert lib.kf_kv_append(ctypes.byref(s), *args) == -2          # fp8 append unsupported
+    s = _shape()
+    bad = [v(FAKE), None] + [v(FAKE)] * 2 + [v(FAKE), 4, v(FAKE), v(FAKE), v(FAKE), None]
+    assert lib.kf_kv_append(ctypes.byref(s), *bad) == -1          # null v_pool
+    bad = [v(FAKE)] * 4 + [v(FAKE), 4, v(FAKE + 1), v(FAKE), v(FAKE), None]
+    assert lib.kf_kv_append(ctypes.byref(s), *bad) == -1          # misaligned tail_route
+    s0 = _shape(num_seqs=0)
+    assert lib.kf_kv_append(ctypes.byref(s0), *([None] * 4 + [None, 0, None, None, None, None])) == 0
+
+
+def test_merge_host_checks(lib):
+    v = ctypes.c_void_p
+    ok = [v(FAKE)] * 7
+    assert lib.kf_merge_partials(2, 4, 8, 64, *ok, None) == -2       # head_dim
+    assert lib.kf_merge_partials(-1, 4, 8, 128, *ok, None) == -1
+    assert lib.kf_merge_partials(2, 4, 8, 128, v(FAKE + 4), *ok[1:], None) == -1  # o_part 8B align
+    assert lib.kf_merge_partials(2, 4, 8, 128, *ok[:2], None, *ok[3:], None) == -1  # null CSR
+    assert lib.kf_merge_partials(0, 4, 8, 128, *([None] * 7), None) == 0
+
+
+def test_workspace_bytes(lib):
+    s = _shape(num_seqs=16, num_q_heads=32, num_kv_heads=8, num_pages=40000, num_page_ids=40000)
+    R, maxp = 64, 513
+    n = kf.partial_attn_workspace_bytes(s, R, maxp)
+    chunks = -(-maxp // 64)
+    units = R * 8
+    recs = units * chunks * 4
+    rup = lambda x: -(-x // 256) * 256  # noqa: E731
+    assert n == rup(units * 4) + rup(recs * 2 * 4) + rup(recs * 128 * 4)
+    assert kf.partial_attn_workspace_bytes(s, -1, 5) == 0
+    assert kf.partial_attn_workspace_bytes(_shape(head_dim=64), 4, 5) == 0

@@ -1,0 +1,191 @@
+"""GPU parity of the HIP path against the fp64 oracle, element by element.
+
+Inputs are seeded synthetic instances of each workload, cut down so that the
+oracle finishes in seconds while still spanning several 4-page tiles, more
+than one 64-page chunk per route (so the cross-workgroup combine runs), and
+ragged last pages.  Every call goes through the C ABI (libkf.so).
+Bars: pools and routes bit-exact; o_part/out max|d| <= 2e-3 and
+rel-L2 <= 1e-3; lse_part/lse max|d| <= 1e-4; equal NaN/-inf positions and
+error flags.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from kf_testlib import compare_all, host, run_gpu, run_oracle, assert_close_o, assert_close_lse
+from kf_workloads import make_instance, workload
+
+pytestmark = [pytest.mark.gpu, pytest.mark.filterwarnings("ignore::RuntimeWarning")]
+
+
+CASES = {
+    # name: (workload, overrides, seq_lens or None, steps)
+    "tiny": ("tiny", {}, None, 1),
+    "tiny_append": ("tiny", dict(appends=1), None, 3),
+    "llama_ragged": ("llama8b_32k", dict(num_seqs=3, part_tokens=1024), [3001, 1700, 4103], 2),
+    "llama_multichunk": ("llama8b_32k", dict(num_seqs=2, part_tokens=2600), [5200, 2611], 2),
+    "agentic_small": ("agentic_mix", dict(num_seqs=6, ctx_range=(100, 6000), part_tokens=2048), None, 2),
+    "million_small": ("million_ctx", dict(num_seqs=2, part_tokens=4096), [20000, 20000], 1),
+    "wide_fp8_small": ("wide_gqa_fp8", dict(num_seqs=3, part_tokens=1024), [3000, 2048, 1111], 1),
+    "mha_g1": ("llama8b_32k", dict(num_seqs=2, num_q_heads=8, num_kv_heads=8, part_tokens=512), [900, 77], 1),
+    "g16": ("llama8b_32k", dict(num_seqs=2, num_q_heads=32, num_kv_heads=2, part_tokens=1000), [1500, 2100], 1),
+    "g8_bf16": ("llama8b_32k", dict(num_seqs=2, num_q_heads=64, num_kv_heads=8, part_tokens=700), [1400, 333], 1),
+    "short_routes": ("llama8b_32k", dict(num_seqs=4, num_q_heads=8, num_kv_heads=2, part_tokens=16), [1, 15, 16, 33], 2),
+}
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_parity(gpu, case):
+    name, over, lens, steps = CASES[case]
+    inst = make_instance(workload(name, **over), seed=1, steps=steps, seq_lens=lens)
+    o = run_oracle(inst, steps)
+    g = host(run_gpu(inst, steps))
+    compare_all(g, o)
+
+
+@pytest.mark.parametrize("seed", [1, 2])
+def test_parity_second_seed(gpu, seed):
+    inst = make_instance(workload("agentic_mix", num_seqs=4, ctx_range=(500, 9000),
+                                  part_tokens=4096), seed=seed, steps=1)
+    compare_all(host(run_gpu(inst, 1)), run_oracle(inst, 1))
+
+
+def test_fp8_second_seed(gpu):
+    inst = make_instance(workload("wide_gqa_fp8", num_seqs=2, part_tokens=2048),
+                         seed=2, seq_lens=[4500, 1234])
+    compare_all(host(run_gpu(inst, 1)), run_oracle(inst, 1))
+
+
+def test_empty_tail_route_then_append(gpu):
+    """A route published at a token boundary starts empty (lse = -inf) and
+    receives the next append (Section 4.2; Section 3.2 step 3)."""
+    wl = workload("llama8b_32k", num_seqs=3, num_q_heads=8, num_kv_heads=2, part_tokens=512)
+    inst = make_instance(wl, seed=3, steps=3, empty_tail=True, seq_lens=[1024, 700, 512])
+    # step 0 without appending: the new routes are empty
+    no_tail = np.full(3, -1, np.int32)
+    o0 = run_oracle(inst, 1, tail_route=no_tail)
+    g0 = host(run_gpu(inst, 1, tail_route=no_tail))
+    assert np.all(np.isneginf(o0["lse_part"][inst.tail_route]))
+    compare_all(g0, o0)
+    compare_all(host(run_gpu(inst, 3)), run_oracle(inst, 3))
+
+
+def test_tail_full_sets_flag_and_leaves_pool(gpu):
+    wl = workload("llama8b_32k", num_seqs=2, num_q_heads=8, num_kv_heads=2, part_tokens=256)
+    inst = make_instance(wl, seed=4, steps=2, seq_lens=[270, 300])  # tails 14 / 44 tokens, cap 1 / 3 pages
+    o = run_oracle(inst, 5)
+    assert o["flags"] == oracle.EFLAG_TAIL_FULL
+    compare_all(host(run_gpu(inst, 5)), o)
+
+
+def test_inactive_and_bad_tail_index(gpu):
+    wl = workload("llama8b_32k", num_seqs=3, num_q_heads=8, num_kv_heads=2, part_tokens=256)
+    inst = make_instance(wl, seed=5, steps=1, seq_lens=[300, 400, 500])
+    tail = inst.tail_route.copy()
+    tail[0] = -1
+    tail[1] = inst.tail_route[2]      # another sequence's route
+    o = run_oracle(inst, 1, tail_route=tail)
+    assert o["flags"] == oracle.EFLAG_BAD_ROUTE
+    compare_all(host(run_gpu(inst, 1, tail_route=tail)), o)
+
+
+def test_bad_route_rows_and_page_ids(gpu):
+    """Device-detected errors: NaN outputs for the affected route/sequence,
+    flags set, nothing read outside the arrays."""
+    import torch
+    from paper_2606_29207_amd.step import DecodeState
+    wl = workload("llama8b_32k", num_seqs=3, num_q_heads=8, num_kv_heads=2, part_tokens=512)
+    inst = make_instance(wl, seed=6, seq_lens=[1300, 900, 700])
+    routes = inst.routes.copy()
+    routes[1, 3] = routes[1, 2] - 5            # tok_end < tok_begin
+    routes[4, 0] = 7                           # seq out of range
+    page_ids = inst.page_ids.copy()
+    page_ids[routes[2, 4] + 1] = inst.num_pages + 3   # page id outside the pool
+    page_ids[routes[5, 4]] = -2
+    args = dict(num_kv_heads=2, scale=inst.scale, max_pages_per_route=inst.max_pages_per_route)
+    o_part, lse_part, f1 = oracle.partial_attn(inst.q, inst.k_pool, inst.v_pool, routes, page_ids, **args)
+    out, lse, f2 = oracle.merge_partials(o_part, lse_part, inst.seq_route_begin)
+    st = DecodeState(q=inst.q, k_pool=inst.k_pool, v_pool=inst.v_pool, routes=routes,
+                     page_ids=page_ids, seq_route_begin=inst.seq_route_begin,
+                     tail_route=inst.tail_route, scale=inst.scale,
+                     max_pages_per_route=inst.max_pages_per_route)
+    st.step()
+    torch.cuda.synchronize()
+    g = host(st)
+    assert g["flags"] == f1 | f2 == oracle.EFLAG_BAD_ROUTE | oracle.EFLAG_BAD_PAGE
+    assert_close_o(g["o_part"], o_part, "o_part")
+    assert_close_lse(g["lse_part"], lse_part, "lse_part")
+    assert_close_o(g["out"], out, "out")
+    assert_close_lse(g["lse"], lse, "lse")
+
+
+def test_bad_csr_row(gpu):
+    import torch
+    from paper_2606_29207_amd import kf
+    R, Hq = 4, 8
+    o_part = torch.randn(R, Hq, 128, device="cuda")
+    lse_part = torch.randn(R, Hq, device="cuda")
+    srb = torch.tensor([0, 2, 1, 4, 9], dtype=torch.int32, device="cuda")
+    out = torch.empty(4, Hq, 128, device="cuda")
+    lse = torch.empty(4, Hq, device="cuda")
+    flags = torch.zeros(1, dtype=torch.int32, device="cuda")
+    kf.merge_partials(4, o_part, lse_part, srb, out, lse, flags)
+    ref_o, ref_l, ref_f = oracle.merge_partials(o_part.cpu().double().numpy(),
+                                                lse_part.cpu().double().numpy(), srb.cpu().numpy())
+    assert int(flags.item()) == ref_f == oracle.EFLAG_BAD_ROUTE
+    assert_close_o(out.cpu().numpy(), ref_o, "out")
+    assert_close_lse(lse.cpu().numpy(), ref_l, "lse")
+
+
+def test_merge_empty_and_no_routes(gpu):
+    import torch
+    from paper_2606_29207_amd import kf
+    Hq = 4
+    o_part = torch.zeros(3, Hq, 128, device="cuda")
+    lse_part = torch.full((3, Hq), float("-inf"), device="cuda")
+    lse_part[2, 1] = 0.5
+    o_part[2, 1] = 3.0
+    srb = torch.tensor([0, 0, 2, 3], dtype=torch.int32, device="cuda")   # seq 0 has no routes
+    out = torch.full((3, Hq, 128), float("nan"), device="cuda")
+    lse = torch.full((3, Hq), float("nan"), device="cuda")
+    flags = torch.zeros(1, dtype=torch.int32, device="cuda")
+    kf.merge_partials(3, o_part, lse_part, srb, out, lse, flags)
+    ref_o, ref_l, _ = oracle.merge_partials(o_part.cpu().double().numpy(),
+                                            lse_part.cpu().double().numpy(), srb.cpu().numpy())
+    assert int(flags.item()) == 0
+    assert_close_o(out.cpu().numpy(), ref_o, "out")
+    assert_close_lse(lse.cpu().numpy(), ref_l, "lse")
+
+
+# ----------------------------------------------------------------- properties
+def test_bitwise_deterministic(gpu):
+    inst = make_instance(workload("llama8b_32k", num_seqs=2, part_tokens=3000), seed=7,
+                         seq_lens=[6000, 4000])
+    a, b = host(run_gpu(inst, 1)), host(run_gpu(inst, 1))
+    for k in ("o_part", "lse_part", "out", "lse", "k_pool", "v_pool", "routes"):
+        assert np.array_equal(a[k], b[k], equal_nan=True), k
+
+
+def test_permuted_pool_is_bitwise_identical(gpu):
+    """Same logical tokens, contiguous vs randomly permuted page table."""
+    over = dict(num_seqs=3, part_tokens=2000)
+    lens = [2500, 4100, 900]
+    a = host(run_gpu(make_instance(workload("llama8b_32k", **over), seed=8, seq_lens=lens), 1))
+    b = host(run_gpu(make_instance(workload("llama8b_32k", permuted=True, **over), seed=8,
+                                   seq_lens=lens), 1))
+    for k in ("o_part", "lse_part", "out", "lse"):
+        assert np.array_equal(a[k], b[k]), k
+
+
+@pytest.mark.parametrize("parts", [512, 1600, 4096])
+def test_split_invariance_against_one_route(gpu, parts):
+    """Section 5.1: the merge over any route split equals attention over the
+    whole range; here GPU merged outputs at several splits against the GPU's
+    own single-route result, and both against the oracle."""
+    lens = [4096, 3000]
+    base = make_instance(workload("llama8b_32k", num_seqs=2, part_tokens=1 << 20), seed=9, seq_lens=lens)
+    split = make_instance(workload("llama8b_32k", num_seqs=2, part_tokens=parts), seed=9, seq_lens=lens)
+    g1, g2 = host(run_gpu(base, 1)), host(run_gpu(split, 1))
+    assert_close_o(g2["out"], g1["out"], "out(split) vs out(1 route)")
+    assert_close_lse(g2["lse"], g1["lse"], "lse(split) vs lse(1 route)")
+    compare_all(g2, run_oracle(split, 1))
