@@ -1,0 +1,272 @@
+"""Benchmark of one decode step of the weightless attention node on one GPU.
+
+A step is the whole hot path over one synthetic batch: tail append of the
+step's K/V token, partial attention of every token-range route, and the
+log-sum-exp merge per sequence, all through the C ABI on one stream.
+Default workload: one Llama-3.1-8B attention layer (16 sequences x 32768
+tokens, 32 query / 8 KV heads, head_dim 128, 4 routes of 8192 tokens per
+sequence, bf16 KV in 16-token pages, one appended token per step).
+
+Prints ONE JSON line: achieved GB/s over the step's algorithmic bytes
+(``value``), microseconds per step, the per-call breakdown, a roofline entry
+for the partial-attention kernel and the fp64 oracle timed on host cores.
+
+Flags: --gpus N (only 1 is supported: the path runs on one GPU)
+       --steps K --warmup W --workload NAME --seed S --no-cpu-baseline
+       --calibrate-copy MiB (time a plain device copy instead; for counter
+       calibration under rocprofv3)
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "achieved HBM GB/s + µs/step for partial decode attn+merge (Llama-3.1-8B layer)"
+HBM_PEAK_GBPS = 8000.0            # MI355X HBM3E, vendor figure
+KERNEL_SRC = os.path.join(ROOT, "paper_2606_29207_amd", "csrc", "kf_kernels.hip")
+COUNTERS = os.path.join(ROOT, "profiles", "partial_kernel_llama8b_32k_counters.md")
+
+
+# ---------------------------------------------------------------- bytes model
+def step_bytes(inst, step: int) -> dict:
+    """Algorithmic HBM bytes of decode step ``step`` (0-based), per call.
+
+    KV bytes follow the footprint formula of the paper's scaling policy
+    (2 * tokens * H_kv * d_h * element bytes per layer); the rest is what each
+    call must read or write at least once."""
+    wl = inst.wl
+    B, Hq, H, D = wl.num_seqs, wl.num_q_heads, wl.num_kv_heads, wl.head_dim
+    esz = 1 if wl.kv_dtype == "fp8" else 2
+    R = len(inst.routes)
+    lens = inst.routes[:, 3].astype(np.int64) - inst.routes[:, 2]
+    if wl.appends:
+        lens = lens.copy()
+        tails = inst.tail_route[inst.tail_route >= 0]
+        lens[tails] += step + 1
+    tokens = int(lens.sum())
+    pages = int((-(-lens // 16)).sum())
+    kv = 2 * tokens * H * D * esz + (2 * pages * H * 4 if esz == 1 else 0)
+    partial = kv + B * Hq * D * 2 + pages * 4 + R * 24 + R * Hq * (D + 1) * 4
+    merge = R * Hq * (D + 1) * 4 + (B + 1) * 4 + B * Hq * (D + 1) * 4
+    n_app = int((inst.tail_route >= 0).sum()) if wl.appends else 0
+    append = 4 * n_app * H * D * 2 + n_app * 24
+    return dict(append=append, partial=partial, merge=merge, kv=kv, tokens=tokens)
+
+
+# --------------------------------------------------------------- cpu baseline
+def cpu_baseline(inst, min_s=10.0, max_s=30.0) -> dict:
+    """The fp64 oracle on the host: partials of (route, KV head) units of the
+    same instance, spread over a thread pool with one BLAS thread each, then
+    the merge of the sequences completed; repeated until ``min_s`` elapses."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    from threadpoolctl import threadpool_limits
+
+    import oracle
+    wl = inst.wl
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count() or 1
+    cores = max(1, min(16, cores))
+    G = wl.group
+
+    def unit(args):
+        r, g = args
+        return oracle.route_partial(inst.q, inst.k_pool, inst.v_pool, inst.routes[r],
+                                    inst.page_ids, g, num_kv_heads=wl.num_kv_heads,
+                                    scale=inst.scale, max_pages_per_route=inst.max_pages_per_route,
+                                    k_scale=inst.k_scale, v_scale=inst.v_scale)
+
+    esz = 1 if wl.kv_dtype == "fp8" else 2
+    done_bytes, done_seqs = 0, 0
+    t0 = time.perf_counter()
+    with threadpool_limits(limits=1), ThreadPoolExecutor(cores) as ex:
+        b = 0
+        while True:
+            rows = range(int(inst.seq_route_begin[b]), int(inst.seq_route_begin[b + 1]))
+            res = list(ex.map(unit, [(r, g) for r in rows for g in range(wl.num_kv_heads)]))
+            o = np.zeros((len(rows), wl.num_q_heads, wl.head_dim))
+            lse = np.zeros((len(rows), wl.num_q_heads))
+            for i, (oo, ll, _) in enumerate(res):
+                r, g = divmod(i, wl.num_kv_heads)
+                o[r, g * G:(g + 1) * G], lse[r, g * G:(g + 1) * G] = oo, ll
+            oracle.merge(o, lse)
+            toks = int((inst.routes[list(rows), 3] - inst.routes[list(rows), 2]).sum())
+            done_bytes += 2 * toks * wl.num_kv_heads * wl.head_dim * esz
+            done_seqs += 1
+            b = (b + 1) % wl.num_seqs
+            el = time.perf_counter() - t0
+            if el >= min_s or el >= max_s:
+                break
+    el = time.perf_counter() - t0
+    return {"value": round(done_bytes / el / 1e9, 4), "unit": "GB/s", "cores": cores,
+            "kind": "oracle",
+            "sample": f"{done_seqs} sequence(s) of the same instance (all routes x KV heads, "
+                      f"fp64 partials + merge, append not timed), {el:.1f} s on {cores} threads, "
+                      f"KV bytes {done_bytes}"}
+
+
+# ------------------------------------------------------------------- counters
+def kernel_hash() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def counter_traffic():
+    """Per-launch HBM bytes of the partial kernel from the committed rocprofv3
+    counter summary, or None when it is absent or the kernel has changed."""
+    if not os.path.exists(COUNTERS):
+        return None
+    txt = open(COUNTERS).read()
+    m = re.search(r"kernel_sha256_16:\s*([0-9a-f]+)", txt)
+    t = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", txt)
+    if not m or not t or m.group(1) != kernel_hash():
+        return None
+    return float(t.group(1))
+
+
+# ------------------------------------------------------------------------ main
+def calibrate_copy(mib: int):
+    import torch
+    n = mib * (1 << 20)
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    print(json.dumps({"copy_bytes_each_way": n, "seconds": dt, "GBps_rw": 2 * n / dt / 1e9}),
+          flush=True)
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama8b_32k")
+    ap.add_argument("--seed", type=int, default=1)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this path runs on exactly one GPU (the decode kernels of one "
+              "attention node); --gpus above 1 is not supported", file=sys.stderr)
+        return 2
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy)
+        return 0
+
+    from kf_workloads import make_instance, workload
+    wl = workload(args.workload)
+    K, W = args.steps, args.warmup
+    t = time.perf_counter()
+    inst = make_instance(wl, seed=args.seed, steps=W + K)
+    print(f"[bench] generated {wl.name} in {time.perf_counter() - t:.1f}s", file=sys.stderr, flush=True)
+
+    cpu = None
+    if not args.no_cpu_baseline:   # host-only work, before the GPU is touched
+        cpu = cpu_baseline(inst)
+        print(f"[bench] cpu baseline {cpu['value']} GB/s on {cpu['cores']} threads",
+              file=sys.stderr, flush=True)
+
+    import torch
+    from paper_2606_29207_amd.step import DecodeState
+    torch.cuda.set_device(0)
+    st = DecodeState.from_instance(inst)
+    news = [st.upload_new_tokens(*inst.new_tokens(s)) if wl.appends else (None, None)
+            for s in range(W + K)]
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+    print(f"[bench] uploaded; warmup {W} steps", file=sys.stderr, flush=True)
+
+    for s in range(W):
+        st.step(*news[s])
+    torch.cuda.synchronize()
+
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        e = ev[i]
+        e[0].record(stream)
+        if wl.appends:
+            st.append(*news[W + i])
+        e[1].record(stream)
+        st.partial()
+        e[2].record(stream)
+        st.merge()
+        e[3].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    flags = st.flags()
+    if flags:
+        print(f"[bench] device error flags {flags}", file=sys.stderr, flush=True)
+        return 1
+
+    t_app = np.array([e[0].elapsed_time(e[1]) for e in ev]) * 1e3      # us
+    t_par = np.array([e[1].elapsed_time(e[2]) for e in ev]) * 1e3
+    t_mrg = np.array([e[2].elapsed_time(e[3]) for e in ev]) * 1e3
+    by = [step_bytes(inst, W + i) for i in range(K)]
+    step_b = np.mean([b["append"] + b["partial"] + b["merge"] for b in by])
+    par_b = np.mean([b["partial"] for b in by])
+    am_b = np.mean([b["partial"] + b["merge"] for b in by])
+    us_step = wall / K * 1e6
+    achieved = par_b / (t_par.mean() * 1e-6) / 1e9
+    traffic = counter_traffic()
+    out = {
+        "metric": METRIC,
+        "value": round(step_b / (us_step * 1e-6) / 1e9, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(us_step / 1e3, 4),
+        "us_per_step": round(us_step, 2),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.kv_dtype == "bf16" else "fp8_e4m3/bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "batch": wl.num_seqs, "q_heads": wl.num_q_heads,
+                   "kv_heads": wl.num_kv_heads, "head_dim": wl.head_dim,
+                   "context": int(inst.seq_lens.max()), "route_tokens": wl.part_tokens,
+                   "routes": int(len(inst.routes)), "page_tokens": 16,
+                   "appends_per_step": wl.appends, "kv_dtype": wl.kv_dtype},
+        "breakdown_us": {"append": round(float(t_app.mean()), 2),
+                         "partial_attn": round(float(t_par.mean()), 2),
+                         "partial_attn_p10_p90": [round(float(np.percentile(t_par, 10)), 2),
+                                                  round(float(np.percentile(t_par, 90)), 2)],
+                         "merge": round(float(t_mrg.mean()), 2)},
+        "attn_merge_us": round(float((t_par + t_mrg).mean()), 2),
+        "attn_merge_GBps": round(am_b / ((t_par + t_mrg).mean() * 1e-6) / 1e9, 2),
+        "bytes_per_step": int(step_b),
+        "roofline": {"bound": "hbm", "kernel": "partial_kernel<bf16>" if wl.kv_dtype == "bf16"
+                     else "partial_kernel<fp8>",
+                     "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": traffic, "algorithmic_bytes_per_launch": int(par_b)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -116,10 +116,12 @@ int kf_kv_append(const kf_shape* shape, void* k_pool, void* v_pool,
 
 /*
  * kf_partial_attn_workspace_bytes -- device scratch kf_partial_attn needs for
- * `num_routes` routes of at most `max_pages_per_route` pages each.  The
- * workspace must be zero-filled before its first use; every call leaves its
- * counter area zero again, so it can be reused across calls and steps.
- * Returns 0 for invalid arguments.
+ * `num_routes` routes of at most `max_pages_per_route` pages each on the
+ * current device (at least 256 bytes).  One workgroup handles a whole
+ * (route, KV head) unit when there are enough units to fill the GPU; with
+ * fewer, each unit is split over several workgroups whose partials go through
+ * this workspace.  No initialisation is needed; contents are dead between
+ * calls.  Returns 0 for invalid arguments.
  */
 size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes,
                                        int32_t max_pages_per_route);

@@ -4,6 +4,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "kf.h"
 #include "kf_internal.h"
 
@@ -35,15 +37,48 @@ hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 
 namespace kf {
 
+namespace {
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_cu_count[kMaxDevices];
+
+// Compute units of the current device (queried once per device; 256 when no
+// device is visible, so that sizes can be computed on a host without a GPU).
+int cu_count() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return 256;
+  }
+  int n = g_cu_count[dev].load(std::memory_order_relaxed);
+  if (n > 0) return n;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) {
+    (void)hipGetLastError();
+    n = 256;
+  }
+  g_cu_count[dev].store(n, std::memory_order_relaxed);
+  return n;
+}
+}  // namespace
+
+int32_t choose_splits(int32_t num_routes, int32_t num_kv_heads, int32_t max_pages_per_route) {
+  const int64_t units = (int64_t)num_routes * num_kv_heads;
+  const int64_t target = 2 * (int64_t)cu_count();  // resident workgroups at two per CU
+  if (units <= 0 || units >= target || max_pages_per_route <= kMinSplitPages) return 1;
+  int64_t s = (target + units - 1) / units;
+  const int64_t smax = (max_pages_per_route + kMinSplitPages - 1) / kMinSplitPages;
+  if (s > smax) s = smax;
+  if (s > 65535) s = 65535;
+  return (int32_t)(s < 1 ? 1 : s);
+}
+
 WorkspaceLayout workspace_layout(int32_t num_routes, int32_t num_kv_heads, int32_t group,
-                                 int32_t max_chunks) {
+                                 int32_t nsplit) {
   WorkspaceLayout l;
-  const size_t units = (size_t)num_routes * num_kv_heads;
-  const size_t recs = units * (size_t)max_chunks * (size_t)group;
-  l.counters_off = 0;
-  l.ml_off = round_up(units * sizeof(int32_t), 256);
-  l.o_off = l.ml_off + round_up(recs * 2 * sizeof(float), 256);
+  const size_t recs = nsplit > 1 ? (size_t)num_routes * num_kv_heads * nsplit * group : 0;
+  l.ml_off = 0;
+  l.o_off = round_up(recs * 2 * sizeof(float), 256);
   l.total = l.o_off + round_up(recs * kDim * sizeof(float), 256);
+  if (l.total < 256) l.total = 256;
   return l;
 }
 
@@ -100,9 +135,8 @@ size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes
                                        int32_t max_pages_per_route) {
   if (check_shape(shape) != KF_OK || num_routes < 0 || max_pages_per_route < 0) return 0;
   const int32_t group = shape->num_q_heads / shape->num_kv_heads;
-  return kf::workspace_layout(num_routes, shape->num_kv_heads, group,
-                              kf::max_chunks_for(max_pages_per_route))
-      .total;
+  const int32_t nsplit = kf::choose_splits(num_routes, shape->num_kv_heads, max_pages_per_route);
+  return kf::workspace_layout(num_routes, shape->num_kv_heads, group, nsplit).total;
 }
 
 int kf_partial_attn(const kf_shape* shape, const void* q, const void* k_pool, const void* v_pool,
@@ -126,9 +160,8 @@ int kf_partial_attn(const kf_shape* shape, const void* q, const void* k_pool, co
   for (const void* p : p4)
     if (p && !aligned(p, 4)) return KF_ERR_INVALID_ARG;
   const int32_t group = shape->num_q_heads / shape->num_kv_heads;
-  const int32_t max_chunks = kf::max_chunks_for(max_pages_per_route);
-  const kf::WorkspaceLayout l =
-      kf::workspace_layout(num_routes, shape->num_kv_heads, group, max_chunks);
+  const int32_t nsplit = kf::choose_splits(num_routes, shape->num_kv_heads, max_pages_per_route);
+  const kf::WorkspaceLayout l = kf::workspace_layout(num_routes, shape->num_kv_heads, group, nsplit);
   if (!workspace || !aligned(workspace, 256) || workspace_bytes < l.total) return KF_ERR_WORKSPACE;
 
   kf::PartialArgs a;
@@ -142,7 +175,6 @@ int kf_partial_attn(const kf_shape* shape, const void* q, const void* k_pool, co
   a.o_part = o_part;
   a.lse_part = lse_part;
   char* ws = static_cast<char*>(workspace);
-  a.counters = reinterpret_cast<int32_t*>(ws + l.counters_off);
   a.ws_ml = reinterpret_cast<float*>(ws + l.ml_off);
   a.ws_o = reinterpret_cast<float*>(ws + l.o_off);
   a.err_flags = err_flags;
@@ -152,7 +184,7 @@ int kf_partial_attn(const kf_shape* shape, const void* q, const void* k_pool, co
   a.group = group;
   a.num_routes = num_routes;
   a.max_pages_per_route = max_pages_per_route;
-  a.max_chunks = max_chunks;
+  a.nsplit = nsplit;
   a.num_pages = shape->num_pages;
   a.num_page_ids = shape->num_page_ids;
   a.scale_log2 = (float)((double)shape->scale * 1.4426950408889634074);

@@ -16,7 +16,7 @@ constexpr int kPage = KF_PAGE_SIZE;   // tokens per page
 constexpr int kDim = KF_HEAD_DIM;     // head dimension
 constexpr int kTilePages = 4;         // pages per wave tile (one lane group per page)
 constexpr int kWaves = 4;             // waves per workgroup
-constexpr int kChunkPages = 64;       // upper bound on pages per workgroup
+constexpr int kMinSplitPages = 16;    // smallest page range a split workgroup gets
 
 struct AppendArgs {
   void* k_pool;
@@ -40,12 +40,11 @@ struct PartialArgs {
   const int32_t* page_ids;
   float* o_part;
   float* lse_part;
-  int32_t* counters;    // [num_routes * Hkv], zero between calls
-  float* ws_ml;         // [num_routes * Hkv * max_chunks][G][2] (max, sum)
-  float* ws_o;          // [num_routes * Hkv * max_chunks][G][kDim]
+  float* ws_ml;         // [num_routes * Hkv * nsplit][G][2] (max, sum); nsplit > 1 only
+  float* ws_o;          // [num_routes * Hkv * nsplit][G][kDim]
   int32_t* err_flags;
   int32_t num_seqs, num_q_heads, num_kv_heads, group;
-  int32_t num_routes, max_pages_per_route, max_chunks;
+  int32_t num_routes, max_pages_per_route, nsplit;
   int32_t num_pages, num_page_ids;
   float scale_log2;     // scale * log2(e): scores are kept in the base-2 domain
 };
@@ -61,15 +60,15 @@ struct MergeArgs {
 };
 
 struct WorkspaceLayout {
-  size_t counters_off, ml_off, o_off, total;
+  size_t ml_off, o_off, total;
 };
 
+// Workgroups per (route, KV head).  One workgroup owns a whole unit unless
+// the units cannot fill the GPU (two resident workgroups per compute unit),
+// in which case each unit's pages are split and a combine kernel follows.
+int32_t choose_splits(int32_t num_routes, int32_t num_kv_heads, int32_t max_pages_per_route);
 WorkspaceLayout workspace_layout(int32_t num_routes, int32_t num_kv_heads, int32_t group,
-                                 int32_t max_chunks);
-inline int32_t max_chunks_for(int32_t max_pages_per_route) {
-  int32_t c = (max_pages_per_route + kChunkPages - 1) / kChunkPages;
-  return c < 1 ? 1 : c;
-}
+                                 int32_t nsplit);
 
 hipError_t launch_append(const AppendArgs& a, hipStream_t stream);
 hipError_t launch_partial(const PartialArgs& a, bool fp8, hipStream_t stream);

@@ -5,8 +5,9 @@
 //   merge_kernel    -- log-sum-exp merge of the partials of each sequence
 //
 // partial_kernel is HBM-bound (4 flop per KV byte at 4 query heads per KV
-// head).  One 256-thread workgroup owns (route, KV head, chunk of <= 64
-// pages); each of its four waves streams 4-page tiles:
+// head).  One 256-thread workgroup owns a (route, KV head) unit -- or, when
+// the units are too few to fill the GPU, one of `nsplit` page ranges of it;
+// each of its four waves streams 4-page tiles:
 //   * lane (grp = lane/16, i = lane%16).  For q.K^T the MFMA A operand row i
 //     is token (page i/4 of the tile, slot 4c + i%4) for c = 0..3, so the
 //     16x16 result lands with lane (grp, head i) holding all 16 scores of
@@ -18,12 +19,15 @@
 //     fill the N = 16 columns (G <= 16, the rest zero).
 //   * p (fp32) enters p.V as bf16 hi + bf16 lo, two MFMAs, so the products
 //     carry ~2^-17 relative error instead of bf16's 2^-9.
+//   * all 32 loads of a tile are issued before any of its arithmetic, and
+//     the page ids of the wave's next tile are fetched a tile ahead.
 //   * softmax state per head is shared by the four lane groups (max reduced
 //     across groups per tile), the running sum is kept per lane and reduced
-//     once at the end.
-// Workgroups of one (route, KV head) write chunk partials to the workspace;
-// the last one to finish (atomic ticket) combines them in chunk order, so
-// results are deterministic and a single kernel produces o_part/lse_part.
+//     once at the end; the four waves are combined through LDS.
+// Workgroups never exchange data with each other inside a kernel: when a
+// unit is split, the split partials go to the workspace and combine_kernel
+// (the next launch on the stream) merges them in split order, so results are
+// deterministic.
 #include "kf_internal.h"
 
 namespace kf {
@@ -36,11 +40,8 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kLn2 = 0.69314718055994530942f;
 constexpr int kThreads = kWaves * 64;
-constexpr int kTilesPerWave = kChunkPages / kTilePages / kWaves;  // 4
 constexpr int kLdsStride = kDim + 4;  // padded row of the per-wave output buffer
 
-static_assert(kTilesPerWave * kTilePages * kWaves == kChunkPages, "chunk must tile evenly");
-static_assert(kTilesPerWave * kTilePages <= 16, "page ids of a wave must fit 16 lanes");
 
 __device__ __forceinline__ float neg_inf() { return -__builtin_inff(); }
 __device__ __forceinline__ float qnan() { return __builtin_nanf(""); }
@@ -122,6 +123,25 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
 }
 
 // ------------------------------------------------------------------ partial
+struct RouteView {
+  int seq, n, npages, base;
+  bool bad;
+};
+
+// Route row r as the kernels see it, with the device-side consistency checks.
+__device__ __forceinline__ RouteView read_route(const PartialArgs& a, int r) {
+  const int32_t* rp = reinterpret_cast<const int32_t*>(a.routes + r);
+  RouteView v;
+  v.seq = rp[0];
+  const int tb = rp[2], te = rp[3], cap = rp[5];
+  v.base = rp[4];
+  v.n = te - tb;
+  v.npages = v.n > 0 ? (v.n + kPage - 1) / kPage : 0;
+  v.bad = v.seq < 0 || v.seq >= a.num_seqs || v.n < 0 || v.base < 0 || v.npages > cap ||
+          v.npages > a.max_pages_per_route || (int64_t)v.base + v.npages > a.num_page_ids;
+  return v;
+}
+
 template <bool FP8>
 __global__ __launch_bounds__(kThreads) void partial_kernel(PartialArgs a) {
   __shared__ float s_o[kWaves][KF_MAX_GROUP][kLdsStride];
@@ -129,50 +149,41 @@ __global__ __launch_bounds__(kThreads) void partial_kernel(PartialArgs a) {
   __shared__ float s_l[kWaves][KF_MAX_GROUP];
   __shared__ float s_fm[KF_MAX_GROUP];
   __shared__ float s_fl[KF_MAX_GROUP];
-  __shared__ int s_last;
 
   const int c = blockIdx.x, g = blockIdx.y, r = blockIdx.z;
   const int G = a.group, Hq = a.num_q_heads, H = a.num_kv_heads;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, grp = lane >> 4, li = lane & 15;
   const int hq0 = g * G;
 
-  const int32_t* rp = reinterpret_cast<const int32_t*>(a.routes + r);
-  const int seq = rp[0], tb = rp[2], te = rp[3], base = rp[4], cap = rp[5];
-  const int n = te - tb;
-  const int npages = n > 0 ? (n + kPage - 1) / kPage : 0;
-  const bool bad = seq < 0 || seq >= a.num_seqs || n < 0 || base < 0 || npages > cap ||
-                   npages > a.max_pages_per_route || (int64_t)base + npages > a.num_page_ids;
-  if (bad || npages == 0) {
+  const RouteView rv = read_route(a, r);
+  if (rv.bad || rv.npages == 0) {
     if (c == 0) {
-      const float ov = bad ? qnan() : 0.0f, lv = bad ? qnan() : neg_inf();
+      const float ov = rv.bad ? qnan() : 0.0f, lv = rv.bad ? qnan() : neg_inf();
       for (int e = tid; e < G * kDim; e += kThreads)
         a.o_part[((size_t)r * Hq + hq0 + e / kDim) * kDim + e % kDim] = ov;
       if (tid < G) a.lse_part[(size_t)r * Hq + hq0 + tid] = lv;
-      if (bad && tid == 0) atomicOr(a.err_flags, KF_EFLAG_BAD_ROUTE);
+      if (rv.bad && tid == 0) atomicOr(a.err_flags, KF_EFLAG_BAD_ROUTE);
     }
     return;
   }
-  const int nchunks = (npages + kChunkPages - 1) / kChunkPages;
-  if (c >= nchunks) return;
-  const int p0 = (int)((int64_t)c * npages / nchunks);
-  const int p1 = (int)((int64_t)(c + 1) * npages / nchunks);
-  const int ntiles = (p1 - p0 + kTilePages - 1) / kTilePages;
-  const int lim = min(n, p1 * kPage);  // route-local token bound of this chunk
+  const int seq = rv.seq, n = rv.n, npages = rv.npages, base = rv.base;
+  const int nsplit = a.nsplit;
+  const int p0 = (int)((int64_t)c * npages / nsplit);
+  const int p1 = (int)((int64_t)(c + 1) * npages / nsplit);
+  const int ntiles = (p1 - p0 + kTilePages - 1) / kTilePages;  // 0 for an empty split
+  const int lim = min(n, p1 * kPage);  // route-local token bound of this range
 
-  // Page ids of this wave's tiles: lane l < 16 holds page (l % 4) of the
-  // wave's tile number l / 4.  Pages past the chunk read page 0 (masked).
-  int my_pid = 0;
+  // Page id of page q of tile tt (page 0 past the range: read, then masked).
   bool pid_bad = false;
-  if (lane < kTilesPerWave * kTilePages) {
-    const int tt = w + kWaves * (lane / kTilePages);
-    const int pg = p0 + tt * kTilePages + lane % kTilePages;
-    if (tt < ntiles && pg < p1) {
-      const int v = a.page_ids[base + pg];
-      if (v < 0 || v >= a.num_pages) pid_bad = true;
-      else my_pid = v;
+  auto page_id = [&](int tt, int q) -> int {
+    const int pg = p0 + tt * kTilePages + q;
+    int v = pg < p1 ? a.page_ids[base + pg] : 0;
+    if (v < 0 || v >= a.num_pages) {
+      pid_bad = true;
+      v = 0;
     }
-  }
-  const bool wave_bad = __ballot(pid_bad) != 0;
+    return v;
+  };
 
   // B operand of q.K^T: query head hq0 + li (zero columns past the group).
   u32x4 qb[4];
@@ -188,12 +199,19 @@ __global__ __launch_bounds__(kThreads) void partial_kernel(PartialArgs a) {
   for (int b8 = 0; b8 < 8; ++b8) oacc[b8] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = neg_inf(), l_run = 0.0f;
 
-  for (int k = 0; k < kTilesPerWave; ++k) {
-    const int tt = w + kWaves * k;
-    if (tt >= ntiles) break;
+  // lane (grp, li) reads K of tile page li/4 and V of tile page grp
+  int next_k = 0, next_v = 0;
+  if (w < ntiles) {
+    next_k = page_id(w, li >> 2);
+    next_v = page_id(w, grp);
+  }
+  for (int tt = w; tt < ntiles; tt += kWaves) {
     const int tp0 = p0 + tt * kTilePages;  // route-local first page of the tile
-    const int pidK = __shfl(my_pid, kTilePages * k + (li >> 2));
-    const int pidV = __shfl(my_pid, kTilePages * k + grp);
+    const int pidK = next_k, pidV = next_v;
+    if (tt + kWaves < ntiles) {
+      next_k = page_id(tt + kWaves, li >> 2);
+      next_v = page_id(tt + kWaves, grp);
+    }
 
     // ---- loads: K rows for q.K^T, V^T rows for p.V
     u32x4 kr[4][4];  // [c][kk]
@@ -212,6 +230,8 @@ __global__ __launch_bounds__(kThreads) void partial_kernel(PartialArgs a) {
         vr[b8][0] = ld16(vb + b8 * 16 * kPage);
         vr[b8][1] = ld16(vb + b8 * 16 * kPage + 8);
       }
+      // keep every load of the tile ahead of the arithmetic that consumes it
+      __builtin_amdgcn_sched_barrier(0);
     } else {
       const uint8_t* kb = static_cast<const uint8_t*>(a.k_pool) +
                           ((size_t)pidK * H + g) * head_elems + (li & 3) * kDim + 16 * grp;
@@ -225,6 +245,8 @@ __global__ __launch_bounds__(kThreads) void partial_kernel(PartialArgs a) {
       u32x4 vc[8];
 #pragma unroll
       for (int b8 = 0; b8 < 8; ++b8) vc[b8] = ld16(vb + b8 * 16 * kPage);
+      // keep every load of the tile ahead of the arithmetic that consumes it
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int cc = 0; cc < 4; ++cc)
 #pragma unroll
@@ -310,7 +332,8 @@ __global__ __launch_bounds__(kThreads) void partial_kernel(PartialArgs a) {
 
   l_run += __shfl_xor(l_run, 16);
   l_run += __shfl_xor(l_run, 32);
-  if (wave_bad) m_run = qnan();
+  const bool wave_bad = __ballot(pid_bad) != 0;
+  if (wave_bad) m_run = qnan();  // a bad page poisons the unit: NaN weights below
 
   // ---- combine the four waves: lane (grp, li) holds d = 16*b8 + 4*grp + r4
   if (li < G) {
@@ -338,9 +361,8 @@ __global__ __launch_bounds__(kThreads) void partial_kernel(PartialArgs a) {
   }
   if (tid == 0 && wave_bad) atomicOr(a.err_flags, KF_EFLAG_BAD_PAGE);
   __syncthreads();
-  // a wave that met a bad page has m = NaN, so its weight poisons the chunk
 
-  if (nchunks == 1) {
+  if (nsplit == 1) {
     for (int e = tid; e < G * kDim; e += kThreads) {
       const int h = e / kDim, d = e % kDim;
       float O = 0.0f;
@@ -352,58 +374,54 @@ __global__ __launch_bounds__(kThreads) void partial_kernel(PartialArgs a) {
       a.lse_part[(size_t)r * Hq + hq0 + tid] = (s_fm[tid] + __log2f(s_fl[tid])) * kLn2;
     return;
   }
-
-  const size_t rec0 = ((size_t)r * H + g) * a.max_chunks;
-  {
-    const size_t rec = rec0 + c;
-    for (int e = tid; e < G * kDim; e += kThreads) {
-      const int h = e / kDim, d = e % kDim;
-      float O = 0.0f;
+  // split unit: unnormalised output and (max, sum) of this page range
+  const size_t rec = ((size_t)r * H + g) * nsplit + c;
+  for (int e = tid; e < G * kDim; e += kThreads) {
+    const int h = e / kDim, d = e % kDim;
+    float O = 0.0f;
 #pragma unroll
-      for (int ww = 0; ww < kWaves; ++ww) O += s_m[ww][h] * s_o[ww][h][d];
-      a.ws_o[(rec * G + h) * kDim + d] = O;
-    }
-    if (tid < G) {
-      a.ws_ml[(rec * G + tid) * 2] = s_fm[tid];
-      a.ws_ml[(rec * G + tid) * 2 + 1] = s_fl[tid];
-    }
+    for (int ww = 0; ww < kWaves; ++ww) O += s_m[ww][h] * s_o[ww][h][d];
+    a.ws_o[(rec * G + h) * kDim + d] = O;
   }
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) {
-    const int old = atomicAdd(a.counters + (size_t)r * H + g, 1);
-    s_last = old == nchunks - 1;
+  if (tid < G) {
+    a.ws_ml[(rec * G + tid) * 2] = s_fm[tid];
+    a.ws_ml[(rec * G + tid) * 2 + 1] = s_fl[tid];
   }
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
+}
 
-  // ---- last workgroup of (route, kv head): combine chunks 0..nchunks-1
+// Combine the split partials of each (route, KV head) in split order.
+__global__ __launch_bounds__(kThreads) void combine_kernel(PartialArgs a) {
+  __shared__ float s_fm[KF_MAX_GROUP];
+  __shared__ float s_fl[KF_MAX_GROUP];
+  const int g = blockIdx.x, r = blockIdx.y, tid = threadIdx.x;
+  const int G = a.group, Hq = a.num_q_heads, H = a.num_kv_heads, nsplit = a.nsplit;
+  const RouteView rv = read_route(a, r);
+  if (rv.bad || rv.npages == 0) return;  // written by partial_kernel
+  const size_t rec0 = ((size_t)r * H + g) * nsplit;
   if (tid < G) {
     float M = neg_inf();
-    for (int cc = 0; cc < nchunks; ++cc) M = fmaxf(M, a.ws_ml[((rec0 + cc) * G + tid) * 2]);
+    for (int c = 0; c < nsplit; ++c) M = fmaxf(M, a.ws_ml[((rec0 + c) * G + tid) * 2]);
     float L = 0.0f;
-    for (int cc = 0; cc < nchunks; ++cc) {
-      const float mc = a.ws_ml[((rec0 + cc) * G + tid) * 2];
-      L += exp2_fast(mc - M) * a.ws_ml[((rec0 + cc) * G + tid) * 2 + 1];
+    for (int c = 0; c < nsplit; ++c) {
+      const float mc = a.ws_ml[((rec0 + c) * G + tid) * 2];
+      if (mc != neg_inf()) L += exp2_fast(mc - M) * a.ws_ml[((rec0 + c) * G + tid) * 2 + 1];
     }
     s_fm[tid] = M;
     s_fl[tid] = L;
   }
   __syncthreads();
+  const int hq0 = g * G;
   for (int e = tid; e < G * kDim; e += kThreads) {
     const int h = e / kDim, d = e % kDim;
     const float M = s_fm[h];
     float O = 0.0f;
-    for (int cc = 0; cc < nchunks; ++cc) {
-      const float mc = a.ws_ml[((rec0 + cc) * G + h) * 2];
-      O += exp2_fast(mc - M) * a.ws_o[((rec0 + cc) * G + h) * kDim + d];
+    for (int c = 0; c < nsplit; ++c) {
+      const float mc = a.ws_ml[((rec0 + c) * G + h) * 2];
+      if (mc != neg_inf()) O += exp2_fast(mc - M) * a.ws_o[((rec0 + c) * G + h) * kDim + d];
     }
     a.o_part[((size_t)r * Hq + hq0 + h) * kDim + d] = O / s_fl[h];
   }
-  if (tid < G)
-    a.lse_part[(size_t)r * Hq + hq0 + tid] = (s_fm[tid] + __log2f(s_fl[tid])) * kLn2;
-  if (tid == 0) a.counters[(size_t)r * H + g] = 0;
+  if (tid < G) a.lse_part[(size_t)r * Hq + hq0 + tid] = (s_fm[tid] + __log2f(s_fl[tid])) * kLn2;
 }
 
 // -------------------------------------------------------------------- merge
@@ -458,11 +476,15 @@ hipError_t launch_append(const AppendArgs& a, hipStream_t stream) {
 
 hipError_t launch_partial(const PartialArgs& a, bool fp8, hipStream_t stream) {
   if (a.num_routes == 0) return hipSuccess;
-  const dim3 grid(a.max_chunks, a.num_kv_heads, a.num_routes);
+  const dim3 grid(a.nsplit, a.num_kv_heads, a.num_routes);
   if (fp8)
     hipLaunchKernelGGL(partial_kernel<true>, grid, dim3(kThreads), 0, stream, a);
   else
     hipLaunchKernelGGL(partial_kernel<false>, grid, dim3(kThreads), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.nsplit == 1) return e;
+  hipLaunchKernelGGL(combine_kernel, dim3(a.num_kv_heads, a.num_routes), dim3(kThreads), 0,
+                     stream, a);
   return hipGetLastError();
 }
 

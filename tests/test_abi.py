@@ -124,13 +124,13 @@ def test_merge_host_checks(lib):
 
 
 def test_workspace_bytes(lib):
-    s = _shape(num_seqs=16, num_q_heads=32, num_kv_heads=8, num_pages=40000, num_page_ids=40000)
-    R, maxp = 64, 513
-    n = kf.partial_attn_workspace_bytes(s, R, maxp)
-    chunks = -(-maxp // 64)
-    units = R * 8
-    recs = units * chunks * 4
+    """Enough (route, KV head) units to fill 256 CUs: no split, minimum size.
+    Four units of 128 pages: 8 splits of 16 pages, records of (o, max, sum)."""
     rup = lambda x: -(-x // 256) * 256  # noqa: E731
-    assert n == rup(units * 4) + rup(recs * 2 * 4) + rup(recs * 128 * 4)
+    s = _shape(num_seqs=16, num_q_heads=32, num_kv_heads=8, num_pages=40000, num_page_ids=40000)
+    assert kf.partial_attn_workspace_bytes(s, 64, 513) == 256
+    s = _shape(num_seqs=1, num_q_heads=8, num_kv_heads=2, num_pages=256, num_page_ids=256)
+    recs = 2 * 2 * 8 * 4
+    assert kf.partial_attn_workspace_bytes(s, 2, 128) == rup(recs * 2 * 4) + rup(recs * 128 * 4)
     assert kf.partial_attn_workspace_bytes(s, -1, 5) == 0
     assert kf.partial_attn_workspace_bytes(_shape(head_dim=64), 4, 5) == 0

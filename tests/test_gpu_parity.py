@@ -1,9 +1,10 @@
 """GPU parity of the HIP path against the fp64 oracle, element by element.
 
 Inputs are seeded synthetic instances of each workload, cut down so that the
-oracle finishes in seconds while still spanning several 4-page tiles, more
-than one 64-page chunk per route (so the cross-workgroup combine runs), and
-ragged last pages.  Every call goes through the C ABI (libkf.so).
+oracle finishes in seconds while still spanning several 4-page tiles and
+ragged last pages.  Small instances have few (route, KV head) units, so each
+unit is split over several workgroups and the combine kernel runs; the
+many_units case has enough units for one workgroup per unit.  Every call goes through the C ABI (libkf.so).
 Bars: pools and routes bit-exact; o_part/out max|d| <= 2e-3 and
 rel-L2 <= 1e-3; lse_part/lse max|d| <= 1e-4; equal NaN/-inf positions and
 error flags.
@@ -30,6 +31,8 @@ CASES = {
     "mha_g1": ("llama8b_32k", dict(num_seqs=2, num_q_heads=8, num_kv_heads=8, part_tokens=512), [900, 77], 1),
     "g16": ("llama8b_32k", dict(num_seqs=2, num_q_heads=32, num_kv_heads=2, part_tokens=1000), [1500, 2100], 1),
     "g8_bf16": ("llama8b_32k", dict(num_seqs=2, num_q_heads=64, num_kv_heads=8, part_tokens=700), [1400, 333], 1),
+    # >= 512 (route, KV head) units: one workgroup per unit, no split
+    "many_units": ("llama8b_32k", dict(part_tokens=256), [300 + 97 * i for i in range(16)], 2),
     "short_routes": ("llama8b_32k", dict(num_seqs=4, num_q_heads=8, num_kv_heads=2, part_tokens=16), [1, 15, 16, 33], 2),
 }
 
