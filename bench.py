@@ -249,7 +249,7 @@ def main(argv=None):
                    "context": int(inst.seq_lens.max()), "route_tokens": wl.part_tokens,
                    "routes": int(len(inst.routes)), "page_tokens": 16,
                    "appends_per_step": wl.appends, "kv_dtype": wl.kv_dtype},
-        "breakdown_us": {"append": round(float(t_app.mean()), 2),
+        "breakdown_us": {"append": round(float(t_app.mean()), 2) if wl.appends else None,
                          "partial_attn": round(float(t_par.mean()), 2),
                          "partial_attn_p10_p90": [round(float(np.percentile(t_par, 10)), 2),
                                                   round(float(np.percentile(t_par, 90)), 2)],
