@@ -14,7 +14,7 @@ namespace kf {
 // sizing on the host.
 constexpr int kPage = KF_PAGE_SIZE;   // tokens per page
 constexpr int kDim = KF_HEAD_DIM;     // head dimension
-constexpr int kTilePages = 4;         // pages per wave tile (one lane group per page)
+constexpr int kTilePages = 2;         // pages per wave tile (two lane groups per page)
 constexpr int kWaves = 4;             // waves per workgroup
 constexpr int kMinSplitPages = 16;    // smallest page range a split workgroup gets
 

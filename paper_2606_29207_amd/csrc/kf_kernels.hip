@@ -37,6 +37,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr float kLn2 = 0.69314718055994530942f;
 constexpr int kThreads = kWaves * 64;
@@ -73,9 +74,29 @@ __device__ __forceinline__ void fp8x16_to_bf16(u32x4 codes, u32x4& lo8, u32x4& h
   hi8 = u32x4{o[4], o[5], o[6], o[7]};
 }
 
+// 8 E4M3FN codes -> one 8-element bf16 operand, exactly.
+__device__ __forceinline__ u32x4 fp8x8_to_bf16(u32x2 codes) {
+  u32x4 o;
+#pragma unroll
+  for (int w = 0; w < 2; ++w) {
+    o[2 * w] = __builtin_bit_cast(uint32_t,
+                                  __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(codes[w], 1.0f, false));
+    o[2 * w + 1] = __builtin_bit_cast(uint32_t,
+                                      __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(codes[w], 1.0f, true));
+  }
+  return o;
+}
+
 template <class T>
 __device__ __forceinline__ u32x4 ld16(const T* p) {
   return *reinterpret_cast<const u32x4*>(p);
+}
+
+// K/V pages are read exactly once per step: stream them with the
+// non-temporal hint so they do not displace reusable lines in the caches.
+template <class T>
+__device__ __forceinline__ u32x4 ld16_stream(const T* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
 }
 
 // ------------------------------------------------------------------- append
@@ -142,8 +163,34 @@ __device__ __forceinline__ RouteView read_route(const PartialArgs& a, int r) {
   return v;
 }
 
+// Raw bytes of one 2-page tile as one lane loads them.
 template <bool FP8>
-__global__ __launch_bounds__(kThreads) void partial_kernel(PartialArgs a) {
+struct TileRaw;
+template <>
+struct TileRaw<false> {
+  u32x4 k[2][4];  // [c][kk]: 8 bf16 of K row (slot of MFMA c), dims 32*kk + 8*grp
+  u32x4 v[8];     // [b8]: 8 bf16 of V^T row d = 16*b8 + li, slots 8*(grp&1) ..
+};
+template <>
+struct TileRaw<true> {
+  u32x4 k[2][2];  // [c][pp]: 16 E4M3 of K row, dims 64*pp + 16*grp ..
+  u32x2 v[8];     // [b8]: 8 E4M3 of V^T row d = 16*b8 + li, slots 8*(grp&1) ..
+};
+
+// Wave-uniform description of one tile: its first route-local page, the
+// page ids of its two pages and, for fp8 pools, their scales.
+template <bool FP8>
+struct TileInfo {
+  int tp0, pid0, pid1;
+};
+template <>
+struct TileInfo<true> {
+  int tp0, pid0, pid1;
+  float ks0, ks1, vs0, vs1;
+};
+
+template <bool FP8>
+__global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
   __shared__ float s_o[kWaves][KF_MAX_GROUP][kLdsStride];
   __shared__ float s_m[kWaves][KF_MAX_GROUP];
   __shared__ float s_l[kWaves][KF_MAX_GROUP];
@@ -152,7 +199,8 @@ __global__ __launch_bounds__(kThreads) void partial_kernel(PartialArgs a) {
 
   const int c = blockIdx.x, g = blockIdx.y, r = blockIdx.z;
   const int G = a.group, Hq = a.num_q_heads, H = a.num_kv_heads;
-  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, grp = lane >> 4, li = lane & 15;
+  const int tid = threadIdx.x, lane = tid & 63, grp = lane >> 4, li = lane & 15;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int hq0 = g * G;
 
   const RouteView rv = read_route(a, r);
@@ -166,23 +214,70 @@ __global__ __launch_bounds__(kThreads) void partial_kernel(PartialArgs a) {
     }
     return;
   }
-  const int seq = rv.seq, n = rv.n, npages = rv.npages, base = rv.base;
+  const int seq = rv.seq, n = rv.n, npages = rv.npages;
   const int nsplit = a.nsplit;
   const int p0 = (int)((int64_t)c * npages / nsplit);
   const int p1 = (int)((int64_t)(c + 1) * npages / nsplit);
   const int ntiles = (p1 - p0 + kTilePages - 1) / kTilePages;  // 0 for an empty split
   const int lim = min(n, p1 * kPage);  // route-local token bound of this range
+  const int nt_w = w < ntiles ? (ntiles - w + kWaves - 1) / kWaves : 0;  // tiles of this wave
+  const int32_t* __restrict__ pids = a.page_ids + rv.base;
 
-  // Page id of page q of tile tt (page 0 past the range: read, then masked).
+  // Tile i of this wave is tile w + kWaves*i of the range.  Page ids are
+  // uniform, so they (and fp8 scales) arrive through scalar loads; a page
+  // past the range or outside the pool reads page 0 and is masked or flagged.
   bool pid_bad = false;
-  auto page_id = [&](int tt, int q) -> int {
-    const int pg = p0 + tt * kTilePages + q;
-    int v = pg < p1 ? a.page_ids[base + pg] : 0;
-    if (v < 0 || v >= a.num_pages) {
-      pid_bad = true;
-      v = 0;
+  auto tile_info = [&](int i) -> TileInfo<FP8> {
+    TileInfo<FP8> t;
+    t.tp0 = p0 + (w + kWaves * i) * kTilePages;
+    const bool two = t.tp0 + 1 < p1;
+    int q0 = pids[t.tp0];
+    int q1 = pids[two ? t.tp0 + 1 : t.tp0];
+    q1 = two ? q1 : 0;
+    if (q0 < 0 || q0 >= a.num_pages) { pid_bad = true; q0 = 0; }
+    if (q1 < 0 || q1 >= a.num_pages) { pid_bad = true; q1 = 0; }
+    t.pid0 = q0;
+    t.pid1 = q1;
+    if constexpr (FP8) {
+      t.ks0 = a.k_scale[(size_t)q0 * H + g];
+      t.ks1 = a.k_scale[(size_t)q1 * H + g];
+      t.vs0 = a.v_scale[(size_t)q0 * H + g];
+      t.vs1 = a.v_scale[(size_t)q1 * H + g];
     }
-    return v;
+    return t;
+  };
+
+  // Lane roles.  q.K^T: A row li is token (tile page li/8, slot
+  // 8*((li/4)&1) + 4c + li%4) of MFMA c; the result gives lane (grp, head li)
+  // slots 8*(grp&1) + 4c + r4 of tile page grp/2, which is exactly the
+  // slot range the lane's p.V operands cover.
+  const int kpage = li >> 3, vpage = grp >> 1;
+  const size_t head_elems = (size_t)kPage * kDim;  // elements of one (page, kv head)
+  const int koff = (8 * ((li >> 2) & 1) + (li & 3)) * kDim + (FP8 ? 16 : 8) * grp;
+  const int voff = li * kPage + 8 * (grp & 1);
+
+  auto issue = [&](TileRaw<FP8>& t, const TileInfo<FP8>& ti) {
+    const size_t hk = ((size_t)(kpage ? ti.pid1 : ti.pid0) * H + g) * head_elems;
+    const size_t hv = ((size_t)(vpage ? ti.pid1 : ti.pid0) * H + g) * head_elems;
+    if constexpr (!FP8) {
+      const uint16_t* kb = static_cast<const uint16_t*>(a.k_pool) + hk + koff;
+      const uint16_t* vb = static_cast<const uint16_t*>(a.v_pool) + hv + voff;
+#pragma unroll
+      for (int cc = 0; cc < 2; ++cc)
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) t.k[cc][kk] = ld16_stream(kb + cc * 4 * kDim + 32 * kk);
+#pragma unroll
+      for (int b8 = 0; b8 < 8; ++b8) t.v[b8] = ld16_stream(vb + b8 * 16 * kPage);
+    } else {
+      const uint8_t* kb = static_cast<const uint8_t*>(a.k_pool) + hk + koff;
+      const uint8_t* vb = static_cast<const uint8_t*>(a.v_pool) + hv + voff;
+#pragma unroll
+      for (int cc = 0; cc < 2; ++cc)
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp) t.k[cc][pp] = ld16_stream(kb + cc * 4 * kDim + 64 * pp);
+#pragma unroll
+      for (int b8 = 0; b8 < 8; ++b8) t.v[b8] = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(vb + b8 * 16 * kPage));
+    }
   };
 
   // B operand of q.K^T: query head hq0 + li (zero columns past the group).
@@ -193,86 +288,46 @@ __global__ __launch_bounds__(kThreads) void partial_kernel(PartialArgs a) {
     qb[kk] = li < G ? ld16(a.q + ((size_t)seq * Hq + hq0 + li) * kDim + d0) : u32x4{0, 0, 0, 0};
   }
 
-  const size_t head_elems = (size_t)kPage * kDim;  // elements of one (page, kv head)
   f32x4 oacc[8];
 #pragma unroll
   for (int b8 = 0; b8 < 8; ++b8) oacc[b8] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = neg_inf(), l_run = 0.0f;
 
-  // lane (grp, li) reads K of tile page li/4 and V of tile page grp
-  int next_k = 0, next_v = 0;
-  if (w < ntiles) {
-    next_k = page_id(w, li >> 2);
-    next_v = page_id(w, grp);
-  }
-  for (int tt = w; tt < ntiles; tt += kWaves) {
-    const int tp0 = p0 + tt * kTilePages;  // route-local first page of the tile
-    const int pidK = next_k, pidV = next_v;
-    if (tt + kWaves < ntiles) {
-      next_k = page_id(tt + kWaves, li >> 2);
-      next_v = page_id(tt + kWaves, grp);
-    }
-
-    // ---- loads: K rows for q.K^T, V^T rows for p.V
-    u32x4 kr[4][4];  // [c][kk]
-    u32x4 vr[8][2];  // [d block][slot half]
+  auto compute = [&](const TileRaw<FP8>& t, const TileInfo<FP8>& ti) {
+    u32x4 kr[2][4], vr[8];
     if constexpr (!FP8) {
-      const uint16_t* kb = static_cast<const uint16_t*>(a.k_pool) +
-                           ((size_t)pidK * H + g) * head_elems + (li & 3) * kDim + 8 * grp;
 #pragma unroll
-      for (int cc = 0; cc < 4; ++cc)
+      for (int cc = 0; cc < 2; ++cc)
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) kr[cc][kk] = ld16(kb + 4 * cc * kDim + 32 * kk);
-      const uint16_t* vb = static_cast<const uint16_t*>(a.v_pool) +
-                           ((size_t)pidV * H + g) * head_elems + li * kPage;
+        for (int kk = 0; kk < 4; ++kk) kr[cc][kk] = t.k[cc][kk];
 #pragma unroll
-      for (int b8 = 0; b8 < 8; ++b8) {
-        vr[b8][0] = ld16(vb + b8 * 16 * kPage);
-        vr[b8][1] = ld16(vb + b8 * 16 * kPage + 8);
-      }
-      // keep every load of the tile ahead of the arithmetic that consumes it
-      __builtin_amdgcn_sched_barrier(0);
+      for (int b8 = 0; b8 < 8; ++b8) vr[b8] = t.v[b8];
     } else {
-      const uint8_t* kb = static_cast<const uint8_t*>(a.k_pool) +
-                          ((size_t)pidK * H + g) * head_elems + (li & 3) * kDim + 16 * grp;
-      u32x4 kc[4][2];
 #pragma unroll
-      for (int cc = 0; cc < 4; ++cc)
+      for (int cc = 0; cc < 2; ++cc)
 #pragma unroll
-        for (int pp = 0; pp < 2; ++pp) kc[cc][pp] = ld16(kb + 4 * cc * kDim + 64 * pp);
-      const uint8_t* vb = static_cast<const uint8_t*>(a.v_pool) +
-                          ((size_t)pidV * H + g) * head_elems + li * kPage;
-      u32x4 vc[8];
+        for (int pp = 0; pp < 2; ++pp) fp8x16_to_bf16(t.k[cc][pp], kr[cc][2 * pp], kr[cc][2 * pp + 1]);
 #pragma unroll
-      for (int b8 = 0; b8 < 8; ++b8) vc[b8] = ld16(vb + b8 * 16 * kPage);
-      // keep every load of the tile ahead of the arithmetic that consumes it
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int cc = 0; cc < 4; ++cc)
-#pragma unroll
-        for (int pp = 0; pp < 2; ++pp) fp8x16_to_bf16(kc[cc][pp], kr[cc][2 * pp], kr[cc][2 * pp + 1]);
-#pragma unroll
-      for (int b8 = 0; b8 < 8; ++b8) fp8x16_to_bf16(vc[b8], vr[b8][0], vr[b8][1]);
+      for (int b8 = 0; b8 < 8; ++b8) vr[b8] = fp8x8_to_bf16(t.v[b8]);
     }
 
-    // ---- S^T = K Q^T: lane (grp, head li) gets slots 4c + r4 of page grp
-    f32x4 s[4];
+    // ---- S^T = K Q^T
+    f32x4 s[2];
 #pragma unroll
-    for (int cc = 0; cc < 4; ++cc) {
+    for (int cc = 0; cc < 2; ++cc) {
       s[cc] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) s[cc] = mfma16(kr[cc][kk], qb[kk], s[cc]);
     }
-
     float ks = a.scale_log2, vs = 1.0f;
     if constexpr (FP8) {
-      ks *= a.k_scale[(size_t)pidV * H + g];
-      vs = a.v_scale[(size_t)pidV * H + g];
+      ks *= vpage ? ti.ks1 : ti.ks0;
+      vs = vpage ? ti.vs1 : ti.vs0;
     }
-    const int tok0 = (tp0 + grp) * kPage;  // route-local token of slot 0 of page grp
+    const int tok0 = (ti.tp0 + vpage) * kPage + 8 * (grp & 1);  // route-local token of slot j = 0
     float mt = neg_inf();
 #pragma unroll
-    for (int cc = 0; cc < 4; ++cc)
+    for (int cc = 0; cc < 2; ++cc)
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4) {
         const float v = (tok0 + 4 * cc + r4 < lim) ? s[cc][r4] * ks : neg_inf();
@@ -288,46 +343,67 @@ __global__ __launch_bounds__(kThreads) void partial_kernel(PartialArgs a) {
 #pragma unroll
     for (int b8 = 0; b8 < 8; ++b8) oacc[b8] *= alpha;
 
-    // ---- P^T operands: slots 8*h2 .. 8*h2+7 of page grp, as bf16 hi + lo
-    u32x4 phi[2], plo[2];
+    // ---- P^T operand: element j = slot 8*(grp&1) + j, as bf16 hi + lo
+    u32x4 phi, plo;
 #pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2) {
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        const int cc = 2 * h2 + (jj >> 1), r4 = 2 * (jj & 1);
-        const float e0 = exp2_fast(s[cc][r4] - m_new);
-        const float e1 = exp2_fast(s[cc][r4 + 1] - m_new);
-        l_run += e0 + e1;
-        const float x0 = e0 * vs, x1 = e1 * vs;
-        const uint32_t b0 = __builtin_bit_cast(uint32_t, x0) & 0xFFFF0000u;
-        const uint32_t b1 = __builtin_bit_cast(uint32_t, x1) & 0xFFFF0000u;
-        phi[h2][jj] = (b0 >> 16) | b1;
-        plo[h2][jj] = pack_bf16_rne(x0 - __builtin_bit_cast(float, b0),
-                                    x1 - __builtin_bit_cast(float, b1));
-      }
+    for (int jj = 0; jj < 4; ++jj) {
+      const int cc = jj >> 1, r4 = 2 * (jj & 1);
+      const float e0 = exp2_fast(s[cc][r4] - m_new);
+      const float e1 = exp2_fast(s[cc][r4 + 1] - m_new);
+      l_run += e0 + e1;
+      const float x0 = e0 * vs, x1 = e1 * vs;
+      const uint32_t b0 = __builtin_bit_cast(uint32_t, x0) & 0xFFFF0000u;
+      const uint32_t b1 = __builtin_bit_cast(uint32_t, x1) & 0xFFFF0000u;
+      phi[jj] = (b0 >> 16) | b1;
+      plo[jj] = pack_bf16_rne(x0 - __builtin_bit_cast(float, b0), x1 - __builtin_bit_cast(float, b1));
     }
 
-    // ---- zero V of slots past the chunk (unused slots may hold anything)
-    if ((tp0 + kTilePages) * kPage > lim) {
+    // ---- zero V of slots past the range (unused slots may hold anything)
+    if ((ti.tp0 + kTilePages) * kPage > lim) {
 #pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2)
+      for (int wd = 0; wd < 4; ++wd) {
+        const int t0 = tok0 + 2 * wd;
+        const uint32_t msk = (t0 < lim ? 0x0000FFFFu : 0u) | (t0 + 1 < lim ? 0xFFFF0000u : 0u);
 #pragma unroll
-        for (int wd = 0; wd < 4; ++wd) {
-          const int t = tok0 + 8 * h2 + 2 * wd;
-          const uint32_t msk = (t < lim ? 0x0000FFFFu : 0u) | (t + 1 < lim ? 0xFFFF0000u : 0u);
-#pragma unroll
-          for (int b8 = 0; b8 < 8; ++b8) vr[b8][h2][wd] &= msk;
-        }
+        for (int b8 = 0; b8 < 8; ++b8) vr[b8][wd] &= msk;
+      }
     }
 
     // ---- O^T += V^T P^T
 #pragma unroll
-    for (int b8 = 0; b8 < 8; ++b8)
-#pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2) {
-        oacc[b8] = mfma16(vr[b8][h2], phi[h2], oacc[b8]);
-        oacc[b8] = mfma16(vr[b8][h2], plo[h2], oacc[b8]);
-      }
+    for (int b8 = 0; b8 < 8; ++b8) {
+      oacc[b8] = mfma16(vr[b8], phi, oacc[b8]);
+      oacc[b8] = mfma16(vr[b8], plo, oacc[b8]);
+    }
+  };
+
+  // ---- two register buffers: while tile i is computed, the loads of tile
+  // i+1 are in flight.  The steady-state loop has no branch between issuing
+  // and computing, so the compiler waits only for the tile it computes.
+  TileRaw<FP8> ra, rb;
+  if (nt_w > 0) {
+    TileInfo<FP8> ia = tile_info(0), ib;
+    issue(ra, ia);
+    int i = 0;
+    for (; i + 2 < nt_w; i += 2) {
+      ib = tile_info(i + 1);
+      issue(rb, ib);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(ra, ia);
+      ia = tile_info(i + 2);
+      issue(ra, ia);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(rb, ib);
+    }
+    if (i + 1 < nt_w) {
+      ib = tile_info(i + 1);
+      issue(rb, ib);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(ra, ia);
+      compute(rb, ib);
+    } else {
+      compute(ra, ia);
+    }
   }
 
   l_run += __shfl_xor(l_run, 16);
