@@ -60,21 +60,28 @@ int cu_count() {
 }
 }  // namespace
 
-int32_t choose_splits(int32_t num_routes, int32_t num_kv_heads, int32_t max_pages_per_route) {
+ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_pages_per_route) {
   const int64_t units = (int64_t)num_routes * num_kv_heads;
-  const int64_t target = 2 * (int64_t)cu_count();  // resident workgroups at two per CU
-  if (units <= 0 || units >= target || max_pages_per_route <= kMinSplitPages) return 1;
-  int64_t s = (target + units - 1) / units;
-  const int64_t smax = (max_pages_per_route + kMinSplitPages - 1) / kMinSplitPages;
-  if (s > smax) s = smax;
-  if (s > 65535) s = 65535;
-  return (int32_t)(s < 1 ? 1 : s);
+  const int64_t slots = 2 * (int64_t)cu_count();  // resident workgroups at two per CU
+  const int32_t whole = max_pages_per_route > 0 ? max_pages_per_route : 1;
+  if (units <= 0 || max_pages_per_route <= kMinSplitPages) return {whole, 1};
+  if (units >= slots && units % slots == 0) return {whole, 1};
+  const int64_t target = units < slots ? slots : 32 * slots;
+  int64_t c = (units * max_pages_per_route + target - 1) / target;
+  if (c < kMinSplitPages) c = kMinSplitPages;
+  if (c >= max_pages_per_route) return {whole, 1};
+  int64_t m = (max_pages_per_route + c - 1) / c;
+  if (m > 65535) {
+    m = 65535;
+    c = (max_pages_per_route + m - 1) / m;
+  }
+  return {(int32_t)c, (int32_t)m};
 }
 
 WorkspaceLayout workspace_layout(int32_t num_routes, int32_t num_kv_heads, int32_t group,
-                                 int32_t nsplit) {
+                                 int32_t max_chunks) {
   WorkspaceLayout l;
-  const size_t recs = nsplit > 1 ? (size_t)num_routes * num_kv_heads * nsplit * group : 0;
+  const size_t recs = max_chunks > 1 ? (size_t)num_routes * num_kv_heads * max_chunks * group : 0;
   l.ml_off = 0;
   l.o_off = round_up(recs * 2 * sizeof(float), 256);
   l.total = l.o_off + round_up(recs * kDim * sizeof(float), 256);
@@ -135,8 +142,8 @@ size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes
                                        int32_t max_pages_per_route) {
   if (check_shape(shape) != KF_OK || num_routes < 0 || max_pages_per_route < 0) return 0;
   const int32_t group = shape->num_q_heads / shape->num_kv_heads;
-  const int32_t nsplit = kf::choose_splits(num_routes, shape->num_kv_heads, max_pages_per_route);
-  return kf::workspace_layout(num_routes, shape->num_kv_heads, group, nsplit).total;
+  const kf::ChunkPlan plan = kf::plan_chunks(num_routes, shape->num_kv_heads, max_pages_per_route);
+  return kf::workspace_layout(num_routes, shape->num_kv_heads, group, plan.max_chunks).total;
 }
 
 int kf_partial_attn(const kf_shape* shape, const void* q, const void* k_pool, const void* v_pool,
@@ -160,8 +167,9 @@ int kf_partial_attn(const kf_shape* shape, const void* q, const void* k_pool, co
   for (const void* p : p4)
     if (p && !aligned(p, 4)) return KF_ERR_INVALID_ARG;
   const int32_t group = shape->num_q_heads / shape->num_kv_heads;
-  const int32_t nsplit = kf::choose_splits(num_routes, shape->num_kv_heads, max_pages_per_route);
-  const kf::WorkspaceLayout l = kf::workspace_layout(num_routes, shape->num_kv_heads, group, nsplit);
+  const kf::ChunkPlan plan = kf::plan_chunks(num_routes, shape->num_kv_heads, max_pages_per_route);
+  const kf::WorkspaceLayout l =
+      kf::workspace_layout(num_routes, shape->num_kv_heads, group, plan.max_chunks);
   if (!workspace || !aligned(workspace, 256) || workspace_bytes < l.total) return KF_ERR_WORKSPACE;
 
   kf::PartialArgs a;
@@ -184,7 +192,8 @@ int kf_partial_attn(const kf_shape* shape, const void* q, const void* k_pool, co
   a.group = group;
   a.num_routes = num_routes;
   a.max_pages_per_route = max_pages_per_route;
-  a.nsplit = nsplit;
+  a.chunk_pages = plan.chunk_pages;
+  a.max_chunks = plan.max_chunks;
   a.num_pages = shape->num_pages;
   a.num_page_ids = shape->num_page_ids;
   a.scale_log2 = (float)((double)shape->scale * 1.4426950408889634074);

@@ -14,7 +14,6 @@ namespace kf {
 // sizing on the host.
 constexpr int kPage = KF_PAGE_SIZE;   // tokens per page
 constexpr int kDim = KF_HEAD_DIM;     // head dimension
-constexpr int kTilePages = 2;         // pages per wave tile (two lane groups per page)
 constexpr int kWaves = 4;             // waves per workgroup
 constexpr int kMinSplitPages = 16;    // smallest page range a split workgroup gets
 
@@ -40,11 +39,12 @@ struct PartialArgs {
   const int32_t* page_ids;
   float* o_part;
   float* lse_part;
-  float* ws_ml;         // [num_routes * Hkv * nsplit][G][2] (max, sum); nsplit > 1 only
-  float* ws_o;          // [num_routes * Hkv * nsplit][G][kDim]
+  float* ws_ml;         // [num_routes * Hkv * max_chunks][G][2] (max, sum); chunked units only
+  float* ws_o;          // [num_routes * Hkv * max_chunks][G][kDim]
   int32_t* err_flags;
   int32_t num_seqs, num_q_heads, num_kv_heads, group;
-  int32_t num_routes, max_pages_per_route, nsplit;
+  int32_t num_routes, max_pages_per_route;
+  int32_t chunk_pages, max_chunks;  // a unit of n pages uses ceil(n / chunk_pages) workgroups
   int32_t num_pages, num_page_ids;
   float scale_log2;     // scale * log2(e): scores are kept in the base-2 domain
 };
@@ -63,12 +63,17 @@ struct WorkspaceLayout {
   size_t ml_off, o_off, total;
 };
 
-// Workgroups per (route, KV head).  One workgroup owns a whole unit unless
-// the units cannot fill the GPU (two resident workgroups per compute unit),
-// in which case each unit's pages are split and a combine kernel follows.
-int32_t choose_splits(int32_t num_routes, int32_t num_kv_heads, int32_t max_pages_per_route);
+// How the pages of each (route, KV head) unit are spread over workgroups.
+// One workgroup owns a whole unit when the units fill whole rounds of the
+// GPU's resident workgroups (two per compute unit); otherwise units are cut
+// into chunks of chunk_pages pages, about 32 chunks per resident slot, so
+// the dispatcher balances uneven routes, and a combine kernel follows.
+struct ChunkPlan {
+  int32_t chunk_pages, max_chunks;
+};
+ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_pages_per_route);
 WorkspaceLayout workspace_layout(int32_t num_routes, int32_t num_kv_heads, int32_t group,
-                                 int32_t nsplit);
+                                 int32_t max_chunks);
 
 hipError_t launch_append(const AppendArgs& a, hipStream_t stream);
 hipError_t launch_partial(const PartialArgs& a, bool fp8, hipStream_t stream);

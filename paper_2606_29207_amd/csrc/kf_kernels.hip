@@ -6,7 +6,7 @@
 //
 // partial_kernel is HBM-bound (4 flop per KV byte at 4 query heads per KV
 // head).  One 256-thread workgroup owns a (route, KV head) unit -- or, when
-// the units are too few to fill the GPU, one of `nsplit` page ranges of it;
+// the host plans chunks, one of its ceil(pages / chunk_pages) page ranges;
 // each of its four waves streams 4-page tiles:
 //   * lane (grp = lane/16, i = lane%16).  For q.K^T the MFMA A operand row i
 //     is token (page i/4 of the tile, slot 4c + i%4) for c = 0..3, so the
@@ -25,9 +25,11 @@
 //     across groups per tile), the running sum is kept per lane and reduced
 //     once at the end; the four waves are combined through LDS.
 // Workgroups never exchange data with each other inside a kernel: when a
-// unit is split, the split partials go to the workspace and combine_kernel
-// (the next launch on the stream) merges them in split order, so results are
+// unit is chunked, the chunk partials go to the workspace and combine_kernel
+// (the next launch on the stream) merges them in chunk order, so results are
 // deterministic.
+#include <type_traits>
+
 #include "kf_internal.h"
 
 namespace kf {
@@ -72,19 +74,6 @@ __device__ __forceinline__ void fp8x16_to_bf16(u32x4 codes, u32x4& lo8, u32x4& h
   }
   lo8 = u32x4{o[0], o[1], o[2], o[3]};
   hi8 = u32x4{o[4], o[5], o[6], o[7]};
-}
-
-// 8 E4M3FN codes -> one 8-element bf16 operand, exactly.
-__device__ __forceinline__ u32x4 fp8x8_to_bf16(u32x2 codes) {
-  u32x4 o;
-#pragma unroll
-  for (int w = 0; w < 2; ++w) {
-    o[2 * w] = __builtin_bit_cast(uint32_t,
-                                  __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(codes[w], 1.0f, false));
-    o[2 * w + 1] = __builtin_bit_cast(uint32_t,
-                                      __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(codes[w], 1.0f, true));
-  }
-  return o;
 }
 
 template <class T>
@@ -163,34 +152,56 @@ __device__ __forceinline__ RouteView read_route(const PartialArgs& a, int r) {
   return v;
 }
 
-// Raw bytes of one 2-page tile as one lane loads them.
+// Tile geometry.  A wave tile is TP pages: 2 for bf16 (16 KiB of K+V), 4 for
+// fp8 (also 16 KiB).  Lane (grp = lane/16, li = lane%16):
+//   q.K^T MFMA c (c < TP) takes K row li = token (kpage(li), kslot(c, li));
+//   the 16x16 result gives lane (grp, head li) the TP*4 slots
+//   vslot0 + 4c + r4 of tile page vpage(grp), which are exactly the k-slots
+//   the lane feeds to p.V (NH = TP/2 MFMAs of 8 slots per 16-dim block).
+template <bool FP8>
+struct Geo {
+  static constexpr int TP = FP8 ? 4 : 2;  // pages per tile
+  static constexpr int NC = TP;           // q.K^T MFMAs of 16 rows per tile
+  static constexpr int NH = TP / 2;       // p.V MFMAs (8 slots each) per 16-dim block
+  static __device__ __forceinline__ int kpage(int li) { return FP8 ? li >> 2 : li >> 3; }
+  static __device__ __forceinline__ int kslot0(int li) {
+    return FP8 ? (li & 3) : 8 * ((li >> 2) & 1) + (li & 3);
+  }
+  static __device__ __forceinline__ int vpage(int grp) { return FP8 ? grp : grp >> 1; }
+  static __device__ __forceinline__ int vslot0(int grp) { return FP8 ? 0 : 8 * (grp & 1); }
+};
+
+// Raw bytes of one tile as one lane loads them.
 template <bool FP8>
 struct TileRaw;
 template <>
 struct TileRaw<false> {
-  u32x4 k[2][4];  // [c][kk]: 8 bf16 of K row (slot of MFMA c), dims 32*kk + 8*grp
-  u32x4 v[8];     // [b8]: 8 bf16 of V^T row d = 16*b8 + li, slots 8*(grp&1) ..
+  u32x4 k[2][4];  // [c][kk]: 8 bf16 of K row kslot(c), dims 32*kk + 8*grp ..
+  u32x4 v[8];     // [b8]: 8 bf16 of V^T row d = 16*b8 + li, slots vslot0 ..
 };
 template <>
 struct TileRaw<true> {
-  u32x4 k[2][2];  // [c][pp]: 16 E4M3 of K row, dims 64*pp + 16*grp ..
-  u32x2 v[8];     // [b8]: 8 E4M3 of V^T row d = 16*b8 + li, slots 8*(grp&1) ..
+  u32x4 k[4][2];  // [c][pp]: 16 E4M3 of K row kslot(c), dims 64*pp + 16*grp ..
+  u32x4 v[8];     // [b8]: the 16 E4M3 slots of V^T row d = 16*b8 + li
 };
 
 // Wave-uniform description of one tile: its first route-local page, the
-// page ids of its two pages and, for fp8 pools, their scales.
-template <bool FP8>
+// page ids of its (up to four) pages and, for fp8 pools, their scales.
 struct TileInfo {
-  int tp0, pid0, pid1;
+  int tp0;
+  int pid0, pid1, pid2, pid3;
+  float ks0, ks1, ks2, ks3, vs0, vs1, vs2, vs3;
 };
-template <>
-struct TileInfo<true> {
-  int tp0, pid0, pid1;
-  float ks0, ks1, vs0, vs1;
-};
+
+template <class T>
+__device__ __forceinline__ T pick4(T v0, T v1, T v2, T v3, int i) {
+  return (i & 2) ? ((i & 1) ? v3 : v2) : ((i & 1) ? v1 : v0);
+}
 
 template <bool FP8>
 __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
+  using GeoT = Geo<FP8>;
+  constexpr int TP = GeoT::TP, NC = GeoT::NC, NH = GeoT::NH;
   __shared__ float s_o[kWaves][KF_MAX_GROUP][kLdsStride];
   __shared__ float s_m[kWaves][KF_MAX_GROUP];
   __shared__ float s_l[kWaves][KF_MAX_GROUP];
@@ -215,10 +226,11 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
     return;
   }
   const int seq = rv.seq, n = rv.n, npages = rv.npages;
-  const int nsplit = a.nsplit;
-  const int p0 = (int)((int64_t)c * npages / nsplit);
-  const int p1 = (int)((int64_t)(c + 1) * npages / nsplit);
-  const int ntiles = (p1 - p0 + kTilePages - 1) / kTilePages;  // 0 for an empty split
+  const int nchunks = (npages + a.chunk_pages - 1) / a.chunk_pages;
+  if (c >= nchunks) return;
+  const int p0 = (int)((int64_t)c * npages / nchunks);
+  const int p1 = (int)((int64_t)(c + 1) * npages / nchunks);
+  const int ntiles = (p1 - p0 + TP - 1) / TP;
   const int lim = min(n, p1 * kPage);  // route-local token bound of this range
   const int nt_w = w < ntiles ? (ntiles - w + kWaves - 1) / kWaves : 0;  // tiles of this wave
   const int32_t* __restrict__ pids = a.page_ids + rv.base;
@@ -227,43 +239,52 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
   // uniform, so they (and fp8 scales) arrive through scalar loads; a page
   // past the range or outside the pool reads page 0 and is masked or flagged.
   bool pid_bad = false;
-  auto tile_info = [&](int i) -> TileInfo<FP8> {
-    TileInfo<FP8> t;
-    t.tp0 = p0 + (w + kWaves * i) * kTilePages;
-    const bool two = t.tp0 + 1 < p1;
-    int q0 = pids[t.tp0];
-    int q1 = pids[two ? t.tp0 + 1 : t.tp0];
-    q1 = two ? q1 : 0;
-    if (q0 < 0 || q0 >= a.num_pages) { pid_bad = true; q0 = 0; }
-    if (q1 < 0 || q1 >= a.num_pages) { pid_bad = true; q1 = 0; }
-    t.pid0 = q0;
-    t.pid1 = q1;
+  auto page_at = [&](int pg) -> int {  // page id of route-local page pg of the range
+    const bool in = pg < p1;
+    int v = pids[in ? pg : p0];
+    v = in ? v : 0;
+    if (v < 0 || v >= a.num_pages) {
+      pid_bad = true;
+      v = 0;
+    }
+    return v;
+  };
+  auto tile_info = [&](int i) -> TileInfo {
+    TileInfo t;
+    t.tp0 = p0 + (w + kWaves * i) * TP;
+    t.pid0 = page_at(t.tp0);
+    t.pid1 = page_at(t.tp0 + 1);
+    t.pid2 = TP > 2 ? page_at(t.tp0 + 2) : 0;
+    t.pid3 = TP > 2 ? page_at(t.tp0 + 3) : 0;
+    t.ks0 = t.ks1 = t.ks2 = t.ks3 = t.vs0 = t.vs1 = t.vs2 = t.vs3 = 1.0f;
     if constexpr (FP8) {
-      t.ks0 = a.k_scale[(size_t)q0 * H + g];
-      t.ks1 = a.k_scale[(size_t)q1 * H + g];
-      t.vs0 = a.v_scale[(size_t)q0 * H + g];
-      t.vs1 = a.v_scale[(size_t)q1 * H + g];
+      t.ks0 = a.k_scale[(size_t)t.pid0 * H + g];
+      t.ks1 = a.k_scale[(size_t)t.pid1 * H + g];
+      t.ks2 = a.k_scale[(size_t)t.pid2 * H + g];
+      t.ks3 = a.k_scale[(size_t)t.pid3 * H + g];
+      t.vs0 = a.v_scale[(size_t)t.pid0 * H + g];
+      t.vs1 = a.v_scale[(size_t)t.pid1 * H + g];
+      t.vs2 = a.v_scale[(size_t)t.pid2 * H + g];
+      t.vs3 = a.v_scale[(size_t)t.pid3 * H + g];
     }
     return t;
   };
 
-  // Lane roles.  q.K^T: A row li is token (tile page li/8, slot
-  // 8*((li/4)&1) + 4c + li%4) of MFMA c; the result gives lane (grp, head li)
-  // slots 8*(grp&1) + 4c + r4 of tile page grp/2, which is exactly the
-  // slot range the lane's p.V operands cover.
-  const int kpage = li >> 3, vpage = grp >> 1;
+  const int kpage = GeoT::kpage(li), vpage = GeoT::vpage(grp);
   const size_t head_elems = (size_t)kPage * kDim;  // elements of one (page, kv head)
-  const int koff = (8 * ((li >> 2) & 1) + (li & 3)) * kDim + (FP8 ? 16 : 8) * grp;
-  const int voff = li * kPage + 8 * (grp & 1);
+  const int koff = GeoT::kslot0(li) * kDim + (FP8 ? 16 : 8) * grp;
+  const int voff = li * kPage + GeoT::vslot0(grp);
 
-  auto issue = [&](TileRaw<FP8>& t, const TileInfo<FP8>& ti) {
-    const size_t hk = ((size_t)(kpage ? ti.pid1 : ti.pid0) * H + g) * head_elems;
-    const size_t hv = ((size_t)(vpage ? ti.pid1 : ti.pid0) * H + g) * head_elems;
+  auto issue = [&](TileRaw<FP8>& t, const TileInfo& ti) {
+    const int pk = pick4(ti.pid0, ti.pid1, ti.pid2, ti.pid3, kpage);
+    const int pv = pick4(ti.pid0, ti.pid1, ti.pid2, ti.pid3, vpage);
+    const size_t hk = ((size_t)pk * H + g) * head_elems;
+    const size_t hv = ((size_t)pv * H + g) * head_elems;
     if constexpr (!FP8) {
       const uint16_t* kb = static_cast<const uint16_t*>(a.k_pool) + hk + koff;
       const uint16_t* vb = static_cast<const uint16_t*>(a.v_pool) + hv + voff;
 #pragma unroll
-      for (int cc = 0; cc < 2; ++cc)
+      for (int cc = 0; cc < NC; ++cc)
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) t.k[cc][kk] = ld16_stream(kb + cc * 4 * kDim + 32 * kk);
 #pragma unroll
@@ -272,11 +293,11 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
       const uint8_t* kb = static_cast<const uint8_t*>(a.k_pool) + hk + koff;
       const uint8_t* vb = static_cast<const uint8_t*>(a.v_pool) + hv + voff;
 #pragma unroll
-      for (int cc = 0; cc < 2; ++cc)
+      for (int cc = 0; cc < NC; ++cc)
 #pragma unroll
         for (int pp = 0; pp < 2; ++pp) t.k[cc][pp] = ld16_stream(kb + cc * 4 * kDim + 64 * pp);
 #pragma unroll
-      for (int b8 = 0; b8 < 8; ++b8) t.v[b8] = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(vb + b8 * 16 * kPage));
+      for (int b8 = 0; b8 < 8; ++b8) t.v[b8] = ld16_stream(vb + b8 * 16 * kPage);
     }
   };
 
@@ -293,41 +314,38 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
   for (int b8 = 0; b8 < 8; ++b8) oacc[b8] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = neg_inf(), l_run = 0.0f;
 
-  auto compute = [&](const TileRaw<FP8>& t, const TileInfo<FP8>& ti) {
-    u32x4 kr[2][4], vr[8];
-    if constexpr (!FP8) {
+  // MASK: the tile may hold slots past the range (only a wave's last tile
+  // can); its V bits are then zeroed.  Kept a compile-time property so the
+  // steady-state loop has no branch.
+  auto compute = [&](const TileRaw<FP8>& t, const TileInfo& ti, auto mask_tag) {
+    constexpr bool MASK = decltype(mask_tag)::value;
+    // ---- S^T = K Q^T (fp8 codes widen to bf16 right before their MFMA)
+    f32x4 s[NC];
 #pragma unroll
-      for (int cc = 0; cc < 2; ++cc)
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk) kr[cc][kk] = t.k[cc][kk];
-#pragma unroll
-      for (int b8 = 0; b8 < 8; ++b8) vr[b8] = t.v[b8];
-    } else {
-#pragma unroll
-      for (int cc = 0; cc < 2; ++cc)
-#pragma unroll
-        for (int pp = 0; pp < 2; ++pp) fp8x16_to_bf16(t.k[cc][pp], kr[cc][2 * pp], kr[cc][2 * pp + 1]);
-#pragma unroll
-      for (int b8 = 0; b8 < 8; ++b8) vr[b8] = fp8x8_to_bf16(t.v[b8]);
-    }
-
-    // ---- S^T = K Q^T
-    f32x4 s[2];
-#pragma unroll
-    for (int cc = 0; cc < 2; ++cc) {
+    for (int cc = 0; cc < NC; ++cc) {
       s[cc] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if constexpr (!FP8) {
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) s[cc] = mfma16(kr[cc][kk], qb[kk], s[cc]);
+        for (int kk = 0; kk < 4; ++kk) s[cc] = mfma16(t.k[cc][kk], qb[kk], s[cc]);
+      } else {
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp) {
+          u32x4 k0, k1;
+          fp8x16_to_bf16(t.k[cc][pp], k0, k1);
+          s[cc] = mfma16(k0, qb[2 * pp], s[cc]);
+          s[cc] = mfma16(k1, qb[2 * pp + 1], s[cc]);
+        }
+      }
     }
     float ks = a.scale_log2, vs = 1.0f;
     if constexpr (FP8) {
-      ks *= vpage ? ti.ks1 : ti.ks0;
-      vs = vpage ? ti.vs1 : ti.vs0;
+      ks *= pick4(ti.ks0, ti.ks1, ti.ks2, ti.ks3, vpage);
+      vs = pick4(ti.vs0, ti.vs1, ti.vs2, ti.vs3, vpage);
     }
-    const int tok0 = (ti.tp0 + vpage) * kPage + 8 * (grp & 1);  // route-local token of slot j = 0
+    const int tok0 = (ti.tp0 + vpage) * kPage + GeoT::vslot0(grp);  // route-local token, c = r4 = 0
     float mt = neg_inf();
 #pragma unroll
-    for (int cc = 0; cc < 2; ++cc)
+    for (int cc = 0; cc < NC; ++cc)
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4) {
         const float v = (tok0 + 4 * cc + r4 < lim) ? s[cc][r4] * ks : neg_inf();
@@ -343,37 +361,51 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
 #pragma unroll
     for (int b8 = 0; b8 < 8; ++b8) oacc[b8] *= alpha;
 
-    // ---- P^T operand: element j = slot 8*(grp&1) + j, as bf16 hi + lo
-    u32x4 phi, plo;
+    // ---- P^T operands: half h2 holds slots 8*h2 + j (j < 8) of the lane's
+    // range, i.e. MFMA c = 2*h2 + j/4, row r4 = j%4; bf16 hi + lo
+    u32x4 phi[NH], plo[NH];
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
-      const int cc = jj >> 1, r4 = 2 * (jj & 1);
-      const float e0 = exp2_fast(s[cc][r4] - m_new);
-      const float e1 = exp2_fast(s[cc][r4 + 1] - m_new);
-      l_run += e0 + e1;
-      const float x0 = e0 * vs, x1 = e1 * vs;
-      const uint32_t b0 = __builtin_bit_cast(uint32_t, x0) & 0xFFFF0000u;
-      const uint32_t b1 = __builtin_bit_cast(uint32_t, x1) & 0xFFFF0000u;
-      phi[jj] = (b0 >> 16) | b1;
-      plo[jj] = pack_bf16_rne(x0 - __builtin_bit_cast(float, b0), x1 - __builtin_bit_cast(float, b1));
-    }
+    for (int h2 = 0; h2 < NH; ++h2)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int cc = 2 * h2 + (jj >> 1), r4 = 2 * (jj & 1);
+        const float e0 = exp2_fast(s[cc][r4] - m_new);
+        const float e1 = exp2_fast(s[cc][r4 + 1] - m_new);
+        l_run += e0 + e1;
+        const float x0 = e0 * vs, x1 = e1 * vs;
+        const uint32_t b0 = __builtin_bit_cast(uint32_t, x0) & 0xFFFF0000u;
+        const uint32_t b1 = __builtin_bit_cast(uint32_t, x1) & 0xFFFF0000u;
+        phi[h2][jj] = (b0 >> 16) | b1;
+        plo[h2][jj] = pack_bf16_rne(x0 - __builtin_bit_cast(float, b0),
+                                    x1 - __builtin_bit_cast(float, b1));
+      }
 
-    // ---- zero V of slots past the range (unused slots may hold anything)
-    if ((ti.tp0 + kTilePages) * kPage > lim) {
+    // ---- O^T += V^T P^T; V of slots past the range is zeroed (unused slots
+    // may hold anything)
+    uint32_t msk[NH][4];
+#pragma unroll
+    for (int h2 = 0; h2 < NH; ++h2)
 #pragma unroll
       for (int wd = 0; wd < 4; ++wd) {
-        const int t0 = tok0 + 2 * wd;
-        const uint32_t msk = (t0 < lim ? 0x0000FFFFu : 0u) | (t0 + 1 < lim ? 0xFFFF0000u : 0u);
-#pragma unroll
-        for (int b8 = 0; b8 < 8; ++b8) vr[b8][wd] &= msk;
+        const int t0 = tok0 + 8 * h2 + 2 * wd;
+        msk[h2][wd] = (t0 < lim ? 0x0000FFFFu : 0u) | (t0 + 1 < lim ? 0xFFFF0000u : 0u);
       }
-    }
-
-    // ---- O^T += V^T P^T
 #pragma unroll
     for (int b8 = 0; b8 < 8; ++b8) {
-      oacc[b8] = mfma16(vr[b8], phi, oacc[b8]);
-      oacc[b8] = mfma16(vr[b8], plo, oacc[b8]);
+      u32x4 vr[NH];
+      if constexpr (!FP8) vr[0] = t.v[b8];
+      else fp8x16_to_bf16(t.v[b8], vr[0], vr[1]);
+      if constexpr (MASK) {
+#pragma unroll
+        for (int h2 = 0; h2 < NH; ++h2)
+#pragma unroll
+          for (int wd = 0; wd < 4; ++wd) vr[h2][wd] &= msk[h2][wd];
+      }
+#pragma unroll
+      for (int h2 = 0; h2 < NH; ++h2) {
+        oacc[b8] = mfma16(vr[h2], phi[h2], oacc[b8]);
+        oacc[b8] = mfma16(vr[h2], plo[h2], oacc[b8]);
+      }
     }
   };
 
@@ -381,28 +413,30 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
   // i+1 are in flight.  The steady-state loop has no branch between issuing
   // and computing, so the compiler waits only for the tile it computes.
   TileRaw<FP8> ra, rb;
+  const std::integral_constant<bool, false> full{};
+  const std::integral_constant<bool, true> masked{};
   if (nt_w > 0) {
-    TileInfo<FP8> ia = tile_info(0), ib;
+    TileInfo ia = tile_info(0), ib;
     issue(ra, ia);
     int i = 0;
     for (; i + 2 < nt_w; i += 2) {
       ib = tile_info(i + 1);
       issue(rb, ib);
       __builtin_amdgcn_sched_barrier(0);
-      compute(ra, ia);
+      compute(ra, ia, full);
       ia = tile_info(i + 2);
       issue(ra, ia);
       __builtin_amdgcn_sched_barrier(0);
-      compute(rb, ib);
+      compute(rb, ib, full);
     }
     if (i + 1 < nt_w) {
       ib = tile_info(i + 1);
       issue(rb, ib);
       __builtin_amdgcn_sched_barrier(0);
-      compute(ra, ia);
-      compute(rb, ib);
+      compute(ra, ia, full);
+      compute(rb, ib, masked);
     } else {
-      compute(ra, ia);
+      compute(ra, ia, masked);
     }
   }
 
@@ -438,7 +472,7 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
   if (tid == 0 && wave_bad) atomicOr(a.err_flags, KF_EFLAG_BAD_PAGE);
   __syncthreads();
 
-  if (nsplit == 1) {
+  if (nchunks == 1) {
     for (int e = tid; e < G * kDim; e += kThreads) {
       const int h = e / kDim, d = e % kDim;
       float O = 0.0f;
@@ -450,8 +484,8 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
       a.lse_part[(size_t)r * Hq + hq0 + tid] = (s_fm[tid] + __log2f(s_fl[tid])) * kLn2;
     return;
   }
-  // split unit: unnormalised output and (max, sum) of this page range
-  const size_t rec = ((size_t)r * H + g) * nsplit + c;
+  // chunked unit: unnormalised output and (max, sum) of this page range
+  const size_t rec = ((size_t)r * H + g) * a.max_chunks + c;
   for (int e = tid; e < G * kDim; e += kThreads) {
     const int h = e / kDim, d = e % kDim;
     float O = 0.0f;
@@ -465,20 +499,22 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
   }
 }
 
-// Combine the split partials of each (route, KV head) in split order.
+// Combine the chunk partials of each chunked (route, KV head) in chunk order.
 __global__ __launch_bounds__(kThreads) void combine_kernel(PartialArgs a) {
   __shared__ float s_fm[KF_MAX_GROUP];
   __shared__ float s_fl[KF_MAX_GROUP];
   const int g = blockIdx.x, r = blockIdx.y, tid = threadIdx.x;
-  const int G = a.group, Hq = a.num_q_heads, H = a.num_kv_heads, nsplit = a.nsplit;
+  const int G = a.group, Hq = a.num_q_heads, H = a.num_kv_heads;
   const RouteView rv = read_route(a, r);
   if (rv.bad || rv.npages == 0) return;  // written by partial_kernel
-  const size_t rec0 = ((size_t)r * H + g) * nsplit;
+  const int nchunks = (rv.npages + a.chunk_pages - 1) / a.chunk_pages;
+  if (nchunks == 1) return;              // written by partial_kernel
+  const size_t rec0 = ((size_t)r * H + g) * a.max_chunks;
   if (tid < G) {
     float M = neg_inf();
-    for (int c = 0; c < nsplit; ++c) M = fmaxf(M, a.ws_ml[((rec0 + c) * G + tid) * 2]);
+    for (int c = 0; c < nchunks; ++c) M = fmaxf(M, a.ws_ml[((rec0 + c) * G + tid) * 2]);
     float L = 0.0f;
-    for (int c = 0; c < nsplit; ++c) {
+    for (int c = 0; c < nchunks; ++c) {
       const float mc = a.ws_ml[((rec0 + c) * G + tid) * 2];
       if (mc != neg_inf()) L += exp2_fast(mc - M) * a.ws_ml[((rec0 + c) * G + tid) * 2 + 1];
     }
@@ -491,7 +527,7 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(PartialArgs a) {
     const int h = e / kDim, d = e % kDim;
     const float M = s_fm[h];
     float O = 0.0f;
-    for (int c = 0; c < nsplit; ++c) {
+    for (int c = 0; c < nchunks; ++c) {
       const float mc = a.ws_ml[((rec0 + c) * G + h) * 2];
       if (mc != neg_inf()) O += exp2_fast(mc - M) * a.ws_o[((rec0 + c) * G + h) * kDim + d];
     }
@@ -552,13 +588,13 @@ hipError_t launch_append(const AppendArgs& a, hipStream_t stream) {
 
 hipError_t launch_partial(const PartialArgs& a, bool fp8, hipStream_t stream) {
   if (a.num_routes == 0) return hipSuccess;
-  const dim3 grid(a.nsplit, a.num_kv_heads, a.num_routes);
+  const dim3 grid(a.max_chunks, a.num_kv_heads, a.num_routes);
   if (fp8)
     hipLaunchKernelGGL(partial_kernel<true>, grid, dim3(kThreads), 0, stream, a);
   else
     hipLaunchKernelGGL(partial_kernel<false>, grid, dim3(kThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.nsplit == 1) return e;
+  if (e != hipSuccess || a.max_chunks == 1) return e;
   hipLaunchKernelGGL(combine_kernel, dim3(a.num_kv_heads, a.num_routes), dim3(kThreads), 0,
                      stream, a);
   return hipGetLastError();

@@ -132,5 +132,11 @@ def test_workspace_bytes(lib):
     s = _shape(num_seqs=1, num_q_heads=8, num_kv_heads=2, num_pages=256, num_page_ids=256)
     recs = 2 * 2 * 8 * 4
     assert kf.partial_attn_workspace_bytes(s, 2, 128) == rup(recs * 2 * 4) + rup(recs * 128 * 4)
+    # 142 routes x 8 KV heads of up to 1025 pages: 1136 units do not fill whole
+    # rounds of 512 resident workgroups -> chunks of ceil(1136*1025/16384) = 72
+    # pages, at most 15 per unit
+    s = _shape(num_seqs=64, num_q_heads=32, num_kv_heads=8, num_pages=10, num_page_ids=10)
+    recs = 142 * 8 * 15 * 4
+    assert kf.partial_attn_workspace_bytes(s, 142, 1025) == rup(recs * 2 * 4) + rup(recs * 128 * 4)
     assert kf.partial_attn_workspace_bytes(s, -1, 5) == 0
     assert kf.partial_attn_workspace_bytes(_shape(head_dim=64), 4, 5) == 0

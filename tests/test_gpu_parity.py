@@ -33,6 +33,9 @@ CASES = {
     "g8_bf16": ("llama8b_32k", dict(num_seqs=2, num_q_heads=64, num_kv_heads=8, part_tokens=700), [1400, 333], 1),
     # >= 512 (route, KV head) units: one workgroup per unit, no split
     "many_units": ("llama8b_32k", dict(part_tokens=256), [300 + 97 * i for i in range(16)], 2),
+    # > 512 units, not a whole number of rounds, uneven routes: chunked units
+    "chunked_uneven": ("llama8b_32k", dict(part_tokens=1024),
+                       [1000 + 523 * i for i in range(16)], 1),
     "short_routes": ("llama8b_32k", dict(num_seqs=4, num_q_heads=8, num_kv_heads=2, part_tokens=16), [1, 15, 16, 33], 2),
 }
 
