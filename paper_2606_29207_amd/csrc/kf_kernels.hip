@@ -5,9 +5,11 @@
 //   merge_kernel    -- log-sum-exp merge of the partials of each sequence
 //
 // partial_kernel is HBM-bound (4 flop per KV byte at 4 query heads per KV
-// head).  One 256-thread workgroup owns a (route, KV head) unit -- or, when
-// the host plans chunks, one of its ceil(pages / chunk_pages) page ranges;
-// each of its four waves streams 4-page tiles:
+// head).  One 256-thread workgroup (four waves, two workgroups per CU) owns a
+// (route, KV head) unit -- or, when the host plans chunks, one of its
+// ceil(pages / chunk_pages) page ranges.  Wave w takes tiles w, w+4, ... of
+// the range, so the summation order is fixed and results are bitwise
+// reproducible.  Each wave streams tiles of 2 (bf16) or 4 (fp8) pages:
 //   * lane (grp = lane/16, i = lane%16).  For q.K^T the MFMA A operand row i
 //     is token (page i/4 of the tile, slot 4c + i%4) for c = 0..3, so the
 //     16x16 result lands with lane (grp, head i) holding all 16 scores of
@@ -31,6 +33,7 @@
 #include <type_traits>
 
 #include "kf_internal.h"
+
 
 namespace kf {
 namespace {
@@ -232,12 +235,13 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
   const int p1 = (int)((int64_t)(c + 1) * npages / nchunks);
   const int ntiles = (p1 - p0 + TP - 1) / TP;
   const int lim = min(n, p1 * kPage);  // route-local token bound of this range
-  const int nt_w = w < ntiles ? (ntiles - w + kWaves - 1) / kWaves : 0;  // tiles of this wave
   const int32_t* __restrict__ pids = a.page_ids + rv.base;
 
-  // Tile i of this wave is tile w + kWaves*i of the range.  Page ids are
-  // uniform, so they (and fp8 scales) arrive through scalar loads; a page
-  // past the range or outside the pool reads page 0 and is masked or flagged.
+  auto next_tile = [&](int cur) -> int { return cur + kWaves; };  // wave w: w, w+4, ...
+
+  // Page ids are uniform, so they (and fp8 scales) arrive through scalar
+  // loads; a page past the range or outside the pool reads page 0 and is
+  // masked or flagged.
   bool pid_bad = false;
   auto page_at = [&](int pg) -> int {  // page id of route-local page pg of the range
     const bool in = pg < p1;
@@ -249,9 +253,9 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
     }
     return v;
   };
-  auto tile_info = [&](int i) -> TileInfo {
+  auto tile_info = [&](int tile) -> TileInfo {  // tile: index within the range
     TileInfo t;
-    t.tp0 = p0 + (w + kWaves * i) * TP;
+    t.tp0 = p0 + tile * TP;
     t.pid0 = page_at(t.tp0);
     t.pid1 = page_at(t.tp0 + 1);
     t.pid2 = TP > 2 ? page_at(t.tp0 + 2) : 0;
@@ -314,9 +318,9 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
   for (int b8 = 0; b8 < 8; ++b8) oacc[b8] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = neg_inf(), l_run = 0.0f;
 
-  // MASK: the tile may hold slots past the range (only a wave's last tile
-  // can); its V bits are then zeroed.  Kept a compile-time property so the
-  // steady-state loop has no branch.
+  // MASK: V bits of slots past the range are zeroed (all ones for a full
+  // tile).  Only a wave's final tile can hold such slots, so masking is a
+  // compile-time property and the steady-state loop has no branch.
   auto compute = [&](const TileRaw<FP8>& t, const TileInfo& ti, auto mask_tag) {
     constexpr bool MASK = decltype(mask_tag)::value;
     // ---- S^T = K Q^T (fp8 codes widen to bf16 right before their MFMA)
@@ -409,35 +413,44 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
     }
   };
 
-  // ---- two register buffers: while tile i is computed, the loads of tile
-  // i+1 are in flight.  The steady-state loop has no branch between issuing
-  // and computing, so the compiler waits only for the tile it computes.
+  // ---- two register buffers: while one tile is computed, the loads of the
+  // wave's next tile are in flight.  Between issuing a tile and computing
+  // the previous one there is no branch, so the compiler waits only for the
+  // tile it computes; tile ids and their page ids are fetched a tile ahead.
+  // Grabs are monotonic, so a tile computed inside the loop always precedes
+  // a tile already handed out and is full; only the exits can hold the
+  // range's last tile and compute masked.
   TileRaw<FP8> ra, rb;
   const std::integral_constant<bool, false> full{};
   const std::integral_constant<bool, true> masked{};
-  if (nt_w > 0) {
-    TileInfo ia = tile_info(0), ib;
+  if (w < ntiles) {
+    const int last = ntiles - 1;
+    TileInfo ia = tile_info(w);
     issue(ra, ia);
-    int i = 0;
-    for (; i + 2 < nt_w; i += 2) {
-      ib = tile_info(i + 1);
+    int tb = next_tile(w);
+    TileInfo ib = tile_info(min(tb, last));
+    bool final_in_b = false;
+    while (true) {
+      if (tb > last) break;
       issue(rb, ib);
+      const int tn = next_tile(tb);
+      const TileInfo in = tile_info(min(tn, last));
       __builtin_amdgcn_sched_barrier(0);
       compute(ra, ia, full);
-      ia = tile_info(i + 2);
+      if (tn > last) {
+        final_in_b = true;
+        break;
+      }
+      ia = in;
       issue(ra, ia);
+      tb = next_tile(tn);
+      const TileInfo in2 = tile_info(min(tb, last));
       __builtin_amdgcn_sched_barrier(0);
       compute(rb, ib, full);
+      ib = in2;
     }
-    if (i + 1 < nt_w) {
-      ib = tile_info(i + 1);
-      issue(rb, ib);
-      __builtin_amdgcn_sched_barrier(0);
-      compute(ra, ia, full);
-      compute(rb, ib, masked);
-    } else {
-      compute(ra, ia, masked);
-    }
+    if (final_in_b) compute(rb, ib, masked);
+    else compute(ra, ia, masked);
   }
 
   l_run += __shfl_xor(l_run, 16);
@@ -445,7 +458,7 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
   const bool wave_bad = __ballot(pid_bad) != 0;
   if (wave_bad) m_run = qnan();  // a bad page poisons the unit: NaN weights below
 
-  // ---- combine the four waves: lane (grp, li) holds d = 16*b8 + 4*grp + r4
+  // ---- combine the waves: lane (grp, li) holds d = 16*b8 + 4*grp + r4
   if (li < G) {
 #pragma unroll
     for (int b8 = 0; b8 < 8; ++b8)
