@@ -15,6 +15,7 @@ Flags: --gpus N (only 1 is supported: the path runs on one GPU)
        --steps K --warmup W --workload NAME --seed S --no-cpu-baseline
        --calibrate-copy MiB (time a plain device copy instead; for counter
        calibration under rocprofv3)
+       --schedule serial|query_first
 """
 from __future__ import annotations
 
@@ -163,6 +164,10 @@ def main(argv=None):
     ap.add_argument("--seed", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB")
+    ap.add_argument("--schedule", choices=("serial", "query_first"), default="serial",
+                    help="serial: append -> partial -> merge on one stream; query_first: "
+                         "historical partials from q alone on one stream, append + tail "
+                         "partials on a second, merge after both")
     args = ap.parse_args(argv)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -196,8 +201,17 @@ def main(argv=None):
     torch.cuda.synchronize()
     print(f"[bench] uploaded; warmup {W} steps", file=sys.stderr, flush=True)
 
+    qf = args.schedule == "query_first"
+    if qf:
+        if not wl.appends:
+            print("bench.py: --schedule query_first needs a workload that appends", file=sys.stderr)
+            return 2
+        st.setup_query_first()
     for s in range(W):
-        st.step(*news[s])
+        if qf:
+            st.step_query_first(*news[s])
+        else:
+            st.step(*news[s])
     torch.cuda.synchronize()
 
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
@@ -206,6 +220,12 @@ def main(argv=None):
     for i in range(K):
         e = ev[i]
         e[0].record(stream)
+        if qf:
+            st.step_query_first(*news[W + i])
+            e[1].record(stream)
+            e[2].record(stream)
+            e[3].record(stream)
+            continue
         if wl.appends:
             st.append(*news[W + i])
         e[1].record(stream)
@@ -220,6 +240,21 @@ def main(argv=None):
         print(f"[bench] device error flags {flags}", file=sys.stderr, flush=True)
         return 1
 
+    if qf:
+        t_step = np.array([e[0].elapsed_time(e[3]) for e in ev]) * 1e3
+        by = [step_bytes(inst, W + i) for i in range(K)]
+        step_b = np.mean([b["append"] + b["partial"] + b["merge"] for b in by])
+        us_step = wall / K * 1e6
+        print(json.dumps({"metric": METRIC, "value": round(step_b / (us_step * 1e-6) / 1e9, 2),
+                          "unit": "GB/s", "n_gpus": 1, "steps": K, "warmup": W,
+                          "ms_per_step": round(us_step / 1e3, 4), "us_per_step": round(us_step, 2),
+                          "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+                          "dtype": "bf16", "data": "synthetic", "schedule": "query_first",
+                          "config": {"workload": wl.name, "batch": wl.num_seqs},
+                          "step_event_us": round(float(t_step.mean()), 2),
+                          "bytes_per_step": int(step_b), "roofline": None, "cpu_baseline": cpu}),
+              flush=True)
+        return 0
     t_app = np.array([e[0].elapsed_time(e[1]) for e in ev]) * 1e3      # us
     t_par = np.array([e[1].elapsed_time(e[2]) for e in ev]) * 1e3
     t_mrg = np.array([e[2].elapsed_time(e[3]) for e in ev]) * 1e3

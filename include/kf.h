@@ -150,6 +150,27 @@ int kf_partial_attn(const kf_shape* shape, const void* q, const void* k_pool,
                     size_t workspace_bytes, int32_t* err_flags, void* stream);
 
 /*
+ * kf_partial_attn_subset -- kf_partial_attn restricted to the routes listed
+ * in route_list[0 .. num_list) (device int32 indices into routes[]); other
+ * rows of o_part/lse_part are left untouched.  With it the step can be
+ * scheduled query-first (Section 5.1): the partials of routes that hold only
+ * historical tokens need nothing but q and can start before the step's new
+ * K/V token exists, while the tail routes append and then attend on another
+ * stream.  Size the workspace with kf_partial_attn_workspace_bytes(shape,
+ * num_list, max_pages_per_route) (any larger count also fits); calls that may
+ * run concurrently need separate workspaces.  A list entry outside [0, num_routes) sets
+ * KF_EFLAG_BAD_ROUTE and writes nothing.  Other arguments, checks and
+ * alignment as for kf_partial_attn (route_list 4-byte aligned).
+ */
+int kf_partial_attn_subset(const kf_shape* shape, const void* q, const void* k_pool,
+                           const void* v_pool, const float* k_scale, const float* v_scale,
+                           const kf_route* routes, int32_t num_routes,
+                           const int32_t* route_list, int32_t num_list,
+                           int32_t max_pages_per_route, const int32_t* page_ids,
+                           float* o_part, float* lse_part, void* workspace,
+                           size_t workspace_bytes, int32_t* err_flags, void* stream);
+
+/*
  * kf_merge_partials -- log-sum-exp merge of the partials of each sequence
  * (Section 3.2, step 4): over the routes r of sequence b,
  *   M = max_r lse_r,  w_r = exp(lse_r - M),

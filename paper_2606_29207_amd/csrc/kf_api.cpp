@@ -146,16 +146,22 @@ size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes
   return kf::workspace_layout(num_routes, shape->num_kv_heads, group, plan.max_chunks).total;
 }
 
-int kf_partial_attn(const kf_shape* shape, const void* q, const void* k_pool, const void* v_pool,
-                    const float* k_scale, const float* v_scale, const kf_route* routes,
-                    int32_t num_routes, int32_t max_pages_per_route, const int32_t* page_ids,
-                    float* o_part, float* lse_part, void* workspace, size_t workspace_bytes,
-                    int32_t* err_flags, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Shared body of kf_partial_attn and kf_partial_attn_subset.
+int partial_attn_impl(const kf_shape* shape, const void* q, const void* k_pool, const void* v_pool,
+                      const float* k_scale, const float* v_scale, const kf_route* routes,
+                      int32_t num_routes, const int32_t* route_list, int32_t num_launch,
+                      int32_t max_pages_per_route, const int32_t* page_ids, float* o_part,
+                      float* lse_part, void* workspace, size_t workspace_bytes,
+                      int32_t* err_flags, void* stream) {
   int st = check_shape(shape);
   if (st != KF_OK) return st;
-  if (num_routes < 0 || max_pages_per_route < 0) return KF_ERR_INVALID_ARG;
-  if (num_routes == 0) return KF_OK;
-  if (num_routes > 65535 || shape->num_kv_heads > 65535) return KF_ERR_UNSUPPORTED;
+  if (num_routes < 0 || num_launch < 0 || max_pages_per_route < 0) return KF_ERR_INVALID_ARG;
+  if (num_launch == 0) return KF_OK;
+  if (num_launch > 65535 || shape->num_kv_heads > 65535) return KF_ERR_UNSUPPORTED;
   const bool fp8 = shape->kv_dtype == KF_KV_FP8_E4M3;
   if (!q || !k_pool || !v_pool || !routes || !o_part || !lse_part || !err_flags ||
       (shape->num_page_ids > 0 && !page_ids))
@@ -163,13 +169,13 @@ int kf_partial_attn(const kf_shape* shape, const void* q, const void* k_pool, co
   if (fp8 && (!k_scale || !v_scale)) return KF_ERR_INVALID_ARG;
   if (!aligned(q, 16) || !aligned(k_pool, 16) || !aligned(v_pool, 16) || !aligned(o_part, 16))
     return KF_ERR_INVALID_ARG;
-  const void* p4[] = {k_scale, v_scale, routes, page_ids, lse_part, err_flags};
+  const void* p4[] = {k_scale, v_scale, routes, route_list, page_ids, lse_part, err_flags};
   for (const void* p : p4)
     if (p && !aligned(p, 4)) return KF_ERR_INVALID_ARG;
   const int32_t group = shape->num_q_heads / shape->num_kv_heads;
-  const kf::ChunkPlan plan = kf::plan_chunks(num_routes, shape->num_kv_heads, max_pages_per_route);
+  const kf::ChunkPlan plan = kf::plan_chunks(num_launch, shape->num_kv_heads, max_pages_per_route);
   const kf::WorkspaceLayout l =
-      kf::workspace_layout(num_routes, shape->num_kv_heads, group, plan.max_chunks);
+      kf::workspace_layout(num_launch, shape->num_kv_heads, group, plan.max_chunks);
   if (!workspace || !aligned(workspace, 256) || workspace_bytes < l.total) return KF_ERR_WORKSPACE;
 
   kf::PartialArgs a;
@@ -179,6 +185,7 @@ int kf_partial_attn(const kf_shape* shape, const void* q, const void* k_pool, co
   a.k_scale = k_scale;
   a.v_scale = v_scale;
   a.routes = routes;
+  a.route_list = route_list;
   a.page_ids = page_ids;
   a.o_part = o_part;
   a.lse_part = lse_part;
@@ -192,12 +199,39 @@ int kf_partial_attn(const kf_shape* shape, const void* q, const void* k_pool, co
   a.group = group;
   a.num_routes = num_routes;
   a.max_pages_per_route = max_pages_per_route;
+  a.num_units_routes = num_launch;
   a.chunk_pages = plan.chunk_pages;
   a.max_chunks = plan.max_chunks;
   a.num_pages = shape->num_pages;
   a.num_page_ids = shape->num_page_ids;
   a.scale_log2 = (float)((double)shape->scale * 1.4426950408889634074);
   return kf::launch_partial(a, fp8, as_stream(stream)) == hipSuccess ? KF_OK : KF_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+int kf_partial_attn(const kf_shape* shape, const void* q, const void* k_pool, const void* v_pool,
+                    const float* k_scale, const float* v_scale, const kf_route* routes,
+                    int32_t num_routes, int32_t max_pages_per_route, const int32_t* page_ids,
+                    float* o_part, float* lse_part, void* workspace, size_t workspace_bytes,
+                    int32_t* err_flags, void* stream) {
+  return partial_attn_impl(shape, q, k_pool, v_pool, k_scale, v_scale, routes, num_routes,
+                           nullptr, num_routes, max_pages_per_route, page_ids, o_part, lse_part,
+                           workspace, workspace_bytes, err_flags, stream);
+}
+
+int kf_partial_attn_subset(const kf_shape* shape, const void* q, const void* k_pool,
+                           const void* v_pool, const float* k_scale, const float* v_scale,
+                           const kf_route* routes, int32_t num_routes, const int32_t* route_list,
+                           int32_t num_list, int32_t max_pages_per_route, const int32_t* page_ids,
+                           float* o_part, float* lse_part, void* workspace,
+                           size_t workspace_bytes, int32_t* err_flags, void* stream) {
+  if (num_list > 0 && !route_list) return KF_ERR_INVALID_ARG;
+  return partial_attn_impl(shape, q, k_pool, v_pool, k_scale, v_scale, routes, num_routes,
+                           route_list, num_list, max_pages_per_route, page_ids, o_part, lse_part,
+                           workspace, workspace_bytes, err_flags, stream);
 }
 
 int kf_merge_partials(int32_t num_seqs, int32_t num_routes, int32_t num_q_heads, int32_t head_dim,

@@ -36,14 +36,16 @@ struct PartialArgs {
   const float* k_scale;
   const float* v_scale;
   const kf_route* routes;
+  const int32_t* route_list;  // routes to process (NULL: all, in order)
   const int32_t* page_ids;
   float* o_part;
   float* lse_part;
-  float* ws_ml;         // [num_routes * Hkv * max_chunks][G][2] (max, sum); chunked units only
-  float* ws_o;          // [num_routes * Hkv * max_chunks][G][kDim]
+  float* ws_ml;         // [launched routes * Hkv * max_chunks][G][2] (max, sum); chunked units only
+  float* ws_o;          // [launched routes * Hkv * max_chunks][G][kDim]
   int32_t* err_flags;
   int32_t num_seqs, num_q_heads, num_kv_heads, group;
   int32_t num_routes, max_pages_per_route;
+  int32_t num_units_routes;  // routes launched: num_list, or num_routes without a list
   int32_t chunk_pages, max_chunks;  // a unit of n pages uses ceil(n / chunk_pages) workgroups
   int32_t num_pages, num_page_ids;
   float scale_log2;     // scale * log2(e): scores are kept in the base-2 domain

@@ -211,12 +211,17 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
   __shared__ float s_fm[KF_MAX_GROUP];
   __shared__ float s_fl[KF_MAX_GROUP];
 
-  const int c = blockIdx.x, g = blockIdx.y, r = blockIdx.z;
+  const int c = blockIdx.x, g = blockIdx.y, u = blockIdx.z;  // u: position in the launch
   const int G = a.group, Hq = a.num_q_heads, H = a.num_kv_heads;
   const int tid = threadIdx.x, lane = tid & 63, grp = lane >> 4, li = lane & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int hq0 = g * G;
 
+  const int r = a.route_list ? a.route_list[u] : u;
+  if (r < 0 || r >= a.num_routes) {  // a list entry naming no route: nothing to write
+    if (c == 0 && g == 0 && tid == 0) atomicOr(a.err_flags, KF_EFLAG_BAD_ROUTE);
+    return;
+  }
   const RouteView rv = read_route(a, r);
   if (rv.bad || rv.npages == 0) {
     if (c == 0) {
@@ -498,7 +503,7 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
     return;
   }
   // chunked unit: unnormalised output and (max, sum) of this page range
-  const size_t rec = ((size_t)r * H + g) * a.max_chunks + c;
+  const size_t rec = ((size_t)u * H + g) * a.max_chunks + c;
   for (int e = tid; e < G * kDim; e += kThreads) {
     const int h = e / kDim, d = e % kDim;
     float O = 0.0f;
@@ -516,13 +521,15 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
 __global__ __launch_bounds__(kThreads) void combine_kernel(PartialArgs a) {
   __shared__ float s_fm[KF_MAX_GROUP];
   __shared__ float s_fl[KF_MAX_GROUP];
-  const int g = blockIdx.x, r = blockIdx.y, tid = threadIdx.x;
+  const int g = blockIdx.x, u = blockIdx.y, tid = threadIdx.x;
   const int G = a.group, Hq = a.num_q_heads, H = a.num_kv_heads;
+  const int r = a.route_list ? a.route_list[u] : u;
+  if (r < 0 || r >= a.num_routes) return;  // flagged by partial_kernel
   const RouteView rv = read_route(a, r);
   if (rv.bad || rv.npages == 0) return;  // written by partial_kernel
   const int nchunks = (rv.npages + a.chunk_pages - 1) / a.chunk_pages;
   if (nchunks == 1) return;              // written by partial_kernel
-  const size_t rec0 = ((size_t)r * H + g) * a.max_chunks;
+  const size_t rec0 = ((size_t)u * H + g) * a.max_chunks;
   if (tid < G) {
     float M = neg_inf();
     for (int c = 0; c < nchunks; ++c) M = fmaxf(M, a.ws_ml[((rec0 + c) * G + tid) * 2]);
@@ -600,15 +607,15 @@ hipError_t launch_append(const AppendArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_partial(const PartialArgs& a, bool fp8, hipStream_t stream) {
-  if (a.num_routes == 0) return hipSuccess;
-  const dim3 grid(a.max_chunks, a.num_kv_heads, a.num_routes);
+  if (a.num_units_routes == 0) return hipSuccess;
+  const dim3 grid(a.max_chunks, a.num_kv_heads, a.num_units_routes);
   if (fp8)
     hipLaunchKernelGGL(partial_kernel<true>, grid, dim3(kThreads), 0, stream, a);
   else
     hipLaunchKernelGGL(partial_kernel<false>, grid, dim3(kThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.max_chunks == 1) return e;
-  hipLaunchKernelGGL(combine_kernel, dim3(a.num_kv_heads, a.num_routes), dim3(kThreads), 0,
+  hipLaunchKernelGGL(combine_kernel, dim3(a.num_kv_heads, a.num_units_routes), dim3(kThreads), 0,
                      stream, a);
   return hipGetLastError();
 }

@@ -26,7 +26,7 @@ EFLAG_BAD_PAGE = 4
 
 # every symbol include/kf.h declares
 EXPORTS = ("kf_kv_append", "kf_partial_attn_workspace_bytes", "kf_partial_attn",
-           "kf_merge_partials", "kf_status_str", "kf_version")
+           "kf_partial_attn_subset", "kf_merge_partials", "kf_status_str", "kf_version")
 
 
 class KFError(RuntimeError):
@@ -66,6 +66,9 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.kf_partial_attn_workspace_bytes.restype = sz
     lib.kf_partial_attn.argtypes = [sp, vp, vp, vp, vp, vp, vp, i32, i32, vp, vp, vp, vp, sz, vp, vp]
     lib.kf_partial_attn.restype = ctypes.c_int
+    lib.kf_partial_attn_subset.argtypes = [sp, vp, vp, vp, vp, vp, vp, i32, vp, i32, i32, vp, vp, vp,
+                                           vp, sz, vp, vp]
+    lib.kf_partial_attn_subset.restype = ctypes.c_int
     lib.kf_merge_partials.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]
     lib.kf_merge_partials.restype = ctypes.c_int
     lib.kf_status_str.argtypes = [ctypes.c_int]
@@ -177,8 +180,10 @@ def alloc_workspace(shape: Shape, num_routes: int, max_pages_per_route: int, dev
 
 def partial_attn(shape: Shape, q, k_pool, v_pool, routes, max_pages_per_route, page_ids,
                  o_part, lse_part, workspace, err_flags, k_scale=None, v_scale=None,
-                 stream=None):
-    """kf_partial_attn.  o_part float32 [R, Hq, 128], lse_part float32 [R, Hq]."""
+                 stream=None, route_list=None):
+    """kf_partial_attn (all routes) or, with ``route_list`` (int32 device
+    tensor of route indices), kf_partial_attn_subset.
+    o_part float32 [R, Hq, 128], lse_part float32 [R, Hq]."""
     lib = load()
     for t, n in ((q, "q"), (k_pool, "k_pool"), (v_pool, "v_pool"), (routes, "routes"),
                  (page_ids, "page_ids"), (o_part, "o_part"), (lse_part, "lse_part"),
@@ -198,12 +203,19 @@ def partial_attn(shape: Shape, q, k_pool, v_pool, routes, max_pages_per_route, p
             _dev(t, n)
             _need(t.dtype == torch.float32 and t.numel() >= shape.num_pages * shape.num_kv_heads,
                   f"{n} must be float32 [num_pages, num_kv_heads]")
-    st = lib.kf_partial_attn(ctypes.byref(shape), _ptr(q), _ptr(k_pool), _ptr(v_pool),
-                             _ptr(k_scale), _ptr(v_scale), _ptr(routes), routes.shape[0],
-                             int(max_pages_per_route), _ptr(page_ids), _ptr(o_part),
-                             _ptr(lse_part), _ptr(workspace), workspace.numel(),
-                             _ptr(err_flags), _stream(stream))
-    _check(st, "kf_partial_attn")
+    common_tail = (int(max_pages_per_route), _ptr(page_ids), _ptr(o_part), _ptr(lse_part),
+                   _ptr(workspace), workspace.numel(), _ptr(err_flags), _stream(stream))
+    if route_list is None:
+        st = lib.kf_partial_attn(ctypes.byref(shape), _ptr(q), _ptr(k_pool), _ptr(v_pool),
+                                 _ptr(k_scale), _ptr(v_scale), _ptr(routes), R, *common_tail)
+        _check(st, "kf_partial_attn")
+    else:
+        _dev(route_list, "route_list")
+        _need(route_list.dtype == torch.int32 and route_list.dim() == 1, "route_list must be int32 [n]")
+        st = lib.kf_partial_attn_subset(ctypes.byref(shape), _ptr(q), _ptr(k_pool), _ptr(v_pool),
+                                        _ptr(k_scale), _ptr(v_scale), _ptr(routes), R,
+                                        _ptr(route_list), route_list.numel(), *common_tail)
+        _check(st, "kf_partial_attn_subset")
 
 
 def merge_partials(num_seqs, o_part, lse_part, seq_route_begin, out, lse_out, err_flags,

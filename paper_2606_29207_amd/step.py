@@ -91,5 +91,44 @@ class DecodeState:
         self.partial(stream)
         self.merge(stream)
 
+    # ----------------------------------------------------- query-first step
+    def setup_query_first(self):
+        """Split the routes into historical ones and the tails (read from the
+        device tail table; call again after editing it) for step_query_first."""
+        tails = self.tail_route.cpu().numpy()
+        tails = np.unique(tails[tails >= 0]).astype(np.int32)
+        R = self.routes.shape[0]
+        hist = np.setdiff1d(np.arange(R, dtype=np.int32), tails).astype(np.int32)
+        self.hist_list = _to_dev(hist, self.device)
+        self.tail_list = _to_dev(tails, self.device)
+        self.ws_hist = kf.alloc_workspace(self.shape, R, self.max_pages_per_route, self.device)
+        self.ws_tail = kf.alloc_workspace(self.shape, R, self.max_pages_per_route, self.device)
+        self.stream_b = torch.cuda.Stream(device=self.device)   # default priority
+        self._qf_ready = torch.cuda.Event()
+        self._qf_tail_done = torch.cuda.Event()
+
+    def step_query_first(self, k_new: torch.Tensor, v_new: torch.Tensor):
+        """One decode step scheduled query-first (Section 5.1): partials of the
+        historical routes start on the current stream from q alone; on a second
+        stream the tails append the new K/V token and then attend; the merge
+        waits for both.  Same kernels as step(), other order."""
+        cur = torch.cuda.current_stream(self.device)
+        self._qf_ready.record(cur)
+        self.stream_b.wait_event(self._qf_ready)
+        if self.hist_list.numel():
+            kf.partial_attn(self.shape, self.q, self.k_pool, self.v_pool, self.routes,
+                            self.max_pages_per_route, self.page_ids, self.o_part, self.lse_part,
+                            self.ws_hist, self.err_flags, self.k_scale, self.v_scale, cur,
+                            route_list=self.hist_list)
+        self.append(k_new, v_new, self.stream_b)
+        if self.tail_list.numel():
+            kf.partial_attn(self.shape, self.q, self.k_pool, self.v_pool, self.routes,
+                            self.max_pages_per_route, self.page_ids, self.o_part, self.lse_part,
+                            self.ws_tail, self.err_flags, self.k_scale, self.v_scale,
+                            self.stream_b, route_list=self.tail_list)
+        self._qf_tail_done.record(self.stream_b)
+        cur.wait_event(self._qf_tail_done)
+        self.merge(cur)
+
     def flags(self) -> int:
         return int(self.err_flags.item())

@@ -95,6 +95,19 @@ def test_partial_attn_host_checks(lib, shape_kw, call_kw, status):
     assert _partial(lib, _shape(**shape_kw), **call_kw) == status
 
 
+def test_partial_attn_subset_host_checks(lib):
+    v = lambda x: None if x is None else ctypes.c_void_p(x)  # noqa: E731
+    s = _shape()
+    base = [v(FAKE)] * 5 + [v(FAKE), 4]
+    tail = [8, v(FAKE), v(FAKE), v(FAKE), v(FAKE), 1 << 30, v(FAKE), None]
+    assert lib.kf_partial_attn_subset(ctypes.byref(s), *base[:3], None, None, v(FAKE), 4,
+                                      None, 3, *tail) == -1          # list missing
+    assert lib.kf_partial_attn_subset(ctypes.byref(s), *base[:3], None, None, v(FAKE), 4,
+                                      v(FAKE + 2), 3, *tail) == -1   # list misaligned
+    assert lib.kf_partial_attn_subset(ctypes.byref(s), *base[:3], None, None, v(FAKE), 4,
+                                      None, 0, *tail) == 0           # empty list: no-op
+
+
 def test_partial_attn_zero_routes_is_a_no_op(lib):
     assert _partial(lib, _shape(), R=0) == 0
 

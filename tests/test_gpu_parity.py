@@ -195,3 +195,53 @@ def test_split_invariance_against_one_route(gpu, parts):
     assert_close_o(g2["out"], g1["out"], "out(split) vs out(1 route)")
     assert_close_lse(g2["lse"], g1["lse"], "lse(split) vs lse(1 route)")
     compare_all(g2, run_oracle(split, 1))
+
+
+# ------------------------------------------------------------ query-first step
+@pytest.mark.parametrize("case", ["llama", "agentic"])
+def test_query_first_step_matches_oracle(gpu, case):
+    """Section 5.1: historical partials from q alone on one stream, append +
+    tail partials on another, merge after both; equal to the serial step."""
+    import torch
+    from paper_2606_29207_amd.step import DecodeState
+    if case == "llama":
+        inst = make_instance(workload("llama8b_32k", num_seqs=3, part_tokens=1024),
+                             seed=11, steps=3, seq_lens=[3001, 1700, 4103])
+    else:
+        inst = make_instance(workload("agentic_mix", num_seqs=5, ctx_range=(300, 5000),
+                                      part_tokens=1024), seed=12, steps=3)
+    st = DecodeState.from_instance(inst)
+    st.setup_query_first()
+    for s_ in range(3):
+        for t in (st.o_part, st.lse_part, st.out, st.lse):
+            t.fill_(float("nan"))
+        st.step_query_first(*st.upload_new_tokens(*inst.new_tokens(s_)))
+    torch.cuda.synchronize()
+    compare_all(host(st), run_oracle(inst, 3))
+
+
+def test_subset_writes_only_listed_rows_and_flags_bad_entries(gpu):
+    import torch
+    from paper_2606_29207_amd import kf
+    from paper_2606_29207_amd.step import DecodeState
+    inst = make_instance(workload("llama8b_32k", num_seqs=2, num_q_heads=8, num_kv_heads=2,
+                                  part_tokens=512), seed=13, seq_lens=[1500, 900])
+    st = DecodeState.from_instance(inst)
+    st.o_part.fill_(7.0)
+    st.lse_part.fill_(7.0)
+    lst = torch.tensor([4, 1, 99], dtype=torch.int32, device="cuda")   # 99: no such route
+    ws = kf.alloc_workspace(st.shape, len(inst.routes), inst.max_pages_per_route)
+    kf.partial_attn(st.shape, st.q, st.k_pool, st.v_pool, st.routes, inst.max_pages_per_route,
+                    st.page_ids, st.o_part, st.lse_part, ws, st.err_flags, route_list=lst)
+    torch.cuda.synchronize()
+    assert st.flags() == oracle.EFLAG_BAD_ROUTE
+    o = st.o_part.cpu().double().numpy()
+    lse = st.lse_part.cpu().double().numpy()
+    ref_o, ref_l, _ = oracle.partial_attn(inst.q, inst.k_pool, inst.v_pool, inst.routes,
+                                          inst.page_ids, num_kv_heads=2, scale=inst.scale,
+                                          max_pages_per_route=inst.max_pages_per_route)
+    listed = [1, 4]
+    others = [r for r in range(len(inst.routes)) if r not in listed]
+    assert_close_o(o[listed], ref_o[listed], "o_part listed")
+    assert_close_lse(lse[listed], ref_l[listed], "lse_part listed")
+    assert np.all(o[others] == 7.0) and np.all(lse[others] == 7.0)
