@@ -106,13 +106,21 @@ enum {
  * an append this step.  Device checks (flag, no write): r < num_routes,
  * routes[r].seq == b, tok_end >= tok_begin, j/16 < page_cap
  * (KF_EFLAG_TAIL_FULL otherwise), page_base + j/16 < num_page_ids, page id in
- * the pool.  Only bf16 pools are supported (KF_ERR_UNSUPPORTED for fp8).
+ * the pool.
+ * bf16 pools: the token's bits are copied; k_scale/v_scale may be NULL.
+ * fp8 pools (the paper has no fp8 KV; this is the library's rule), per page
+ * and KV head, separately for K and V, in float32: the first token of a page
+ * sets scale = amax/28 (1 if amax = 0), i.e. 16x headroom below 448; a later
+ * token whose amax exceeds 448*scale first re-encodes the page's earlier
+ * slots to scale' = amax/28 (code' = RNE(decode(code)*scale/scale')); the
+ * token is stored as the E4M3 code nearest to x/scale (ties to even, clamped
+ * to +-448).
  * Alignment: every pointer 4-byte aligned.
  */
-int kf_kv_append(const kf_shape* shape, void* k_pool, void* v_pool,
-                 const void* k_new, const void* v_new, kf_route* routes,
-                 int32_t num_routes, const int32_t* tail_route,
-                 const int32_t* page_ids, int32_t* err_flags, void* stream);
+int kf_kv_append(const kf_shape* shape, void* k_pool, void* v_pool, float* k_scale,
+                 float* v_scale, const void* k_new, const void* v_new, kf_route* routes,
+                 int32_t num_routes, const int32_t* tail_route, const int32_t* page_ids,
+                 int32_t* err_flags, void* stream);
 
 /*
  * kf_partial_attn_workspace_bytes -- device scratch kf_partial_attn needs for

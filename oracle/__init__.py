@@ -18,6 +18,7 @@ from .kf_oracle import (  # noqa: F401
     bf16_to_f64,
     e4m3_table,
     e4m3_to_f64,
+    e4m3_encode_rne,
     gather_kv,
     attend,
     route_partial,

@@ -73,6 +73,25 @@ def e4m3_to_f64(codes) -> np.ndarray:
     return _E4M3[np.asarray(codes, dtype=np.uint8)]
 
 
+_E4M3_POS = _E4M3[:0x7F]          # codes 0x00..0x7E: 0 .. 448, increasing
+
+
+def e4m3_encode_rne(x) -> np.ndarray:
+    """Nearest E4M3FN code to each value (ties to the even code), after
+    clamping to [-448, 448]: the format's definition of round-to-nearest-even
+    applied to the 127 non-negative grid values; the sign bit is the value's
+    (a negative value that rounds to zero gives -0, code 0x80)."""
+    x = np.asarray(x, dtype=np.float64)
+    a = np.minimum(np.abs(x), 448.0)
+    hi = np.searchsorted(_E4M3_POS, a, side="left")          # first grid value >= a
+    hi = np.minimum(hi, 0x7E)
+    lo = np.maximum(hi - 1, 0)
+    dlo, dhi = a - _E4M3_POS[lo], _E4M3_POS[hi] - a
+    pick_hi = (dhi < dlo) | ((dhi == dlo) & (hi % 2 == 0))
+    code = np.where(a == _E4M3_POS[hi], hi, np.where(pick_hi, hi, lo)).astype(np.uint8)
+    return (code | (np.signbit(x).astype(np.uint8) << 7)).astype(np.uint8)
+
+
 # -------------------------------------------------------------------- gather
 def gather_kv(route, page_ids, k_pool, v_pool, kv_head, k_scale=None, v_scale=None):
     """Logical K, V [n, d] (fp64) of one route and KV head.
@@ -209,15 +228,32 @@ def merge_partials(o_part, lse_part, seq_route_begin):
 
 
 # -------------------------------------------------------------------- append
-def kv_append(k_pool, v_pool, routes, page_ids, tail_route, k_new, v_new):
+def kv_append(k_pool, v_pool, routes, page_ids, tail_route, k_new, v_new,
+              k_scale=None, v_scale=None):
     """Tail append (Section 3.2, step 3; Section 5.1): each sequence b with a
     tail route r = tail_route[b] >= 0 stores its new K/V token (bf16 bits
     [B, Hkv, d]) at local index j = tok_end - tok_begin of route r and then
     extends the route by one token.  Works on copies; returns
-    (k_pool, v_pool, routes, flags).  A full tail (no reserved page for j)
-    or an inconsistent route leaves that sequence unchanged and sets a flag."""
+    (k_pool, v_pool, routes, flags) for bf16 pools and
+    (k_pool, v_pool, k_scale, v_scale, routes, flags) for E4M3 pools.  A full
+    tail (no reserved page for j) or an inconsistent route leaves that
+    sequence unchanged and sets a flag.
+
+    E4M3 pools (no fp8 KV in the paper; this build's reading), per page and KV
+    head, separately for K and V, in float32 arithmetic:
+      * the first token of a page sets scale = amax/28 (1 if amax = 0): its
+        largest element lands at 28 = 448/16, leaving 16x headroom, which
+        costs no precision (E4M3 keeps 3 mantissa bits in every normal binade);
+      * a later token whose amax exceeds 448*scale first re-encodes the
+        page's earlier slots to scale' = amax/28 (value = decode(code)*scale,
+        code' = RNE(value/scale')), then the scale becomes scale';
+      * the token is stored as RNE(x/scale), clamped to +-448."""
+    fp8 = k_pool.dtype == np.uint8
     k_pool = k_pool.copy()
     v_pool = v_pool.copy()
+    if fp8:
+        k_scale = np.array(k_scale, dtype=np.float32, copy=True)
+        v_scale = np.array(v_scale, dtype=np.float32, copy=True)
     routes = np.array(routes, dtype=np.int32, copy=True)
     R = len(routes)
     P = k_pool.shape[0]
@@ -241,10 +277,45 @@ def kv_append(k_pool, v_pool, routes, page_ids, tail_route, k_new, v_new):
         if not 0 <= pid < P:
             flags |= EFLAG_BAD_PAGE
             continue
-        k_pool[pid, :, j % PAGE, :] = k_new[b]
-        v_pool[pid, :, :, j % PAGE] = v_new[b]
+        slot = j % PAGE
+        if fp8:
+            for g in range(k_pool.shape[1]):
+                _append_e4m3(k_pool[pid, g], k_scale, pid, g, slot, k_new[b, g], kmajor=True)
+                _append_e4m3(v_pool[pid, g], v_scale, pid, g, slot, v_new[b, g], kmajor=False)
+        else:
+            k_pool[pid, :, slot, :] = k_new[b]
+            v_pool[pid, :, :, slot] = v_new[b]
         routes[r, 3] = te + 1
+    if fp8:
+        return k_pool, v_pool, k_scale, v_scale, routes, flags
     return k_pool, v_pool, routes, flags
+
+
+def _append_e4m3(page, scales, pid, g, slot, x_bits, kmajor):
+    """One (page, KV head) of an E4M3 pool: page is [16, d] (K) or [d, 16] (V)."""
+    f32 = np.float32
+    x = (np.asarray(x_bits, np.uint16).astype(np.uint32) << 16).view(np.float32)
+    amax = f32(np.max(np.abs(x)))
+    if slot == 0:
+        scale = f32(amax / f32(28.0)) if amax > 0 else f32(1.0)
+    else:
+        scale = f32(scales[pid, g])
+        if amax > f32(f32(448.0) * scale):
+            new = f32(amax / f32(28.0))
+            old = page[:slot, :] if kmajor else page[:, :slot]
+            vals = (e4m3_to_f64(old).astype(np.float32) * scale).astype(np.float32)
+            recoded = e4m3_encode_rne((vals / new).astype(np.float32))
+            if kmajor:
+                page[:slot, :] = recoded
+            else:
+                page[:, :slot] = recoded
+            scale = new
+    scales[pid, g] = scale
+    codes = e4m3_encode_rne((x / scale).astype(np.float32))
+    if kmajor:
+        page[slot, :] = codes
+    else:
+        page[:, slot] = codes
 
 
 # --------------------------------------------------------------------- bytes

@@ -106,24 +106,28 @@ const char* kf_status_str(int status) {
 
 const char* kf_version(void) { return "kf 0.1 gfx950"; }
 
-int kf_kv_append(const kf_shape* shape, void* k_pool, void* v_pool, const void* k_new,
-                 const void* v_new, kf_route* routes, int32_t num_routes,
-                 const int32_t* tail_route, const int32_t* page_ids, int32_t* err_flags,
-                 void* stream) {
+int kf_kv_append(const kf_shape* shape, void* k_pool, void* v_pool, float* k_scale,
+                 float* v_scale, const void* k_new, const void* v_new, kf_route* routes,
+                 int32_t num_routes, const int32_t* tail_route, const int32_t* page_ids,
+                 int32_t* err_flags, void* stream) {
   int st = check_shape(shape);
   if (st != KF_OK) return st;
-  if (shape->kv_dtype != KF_KV_BF16) return KF_ERR_UNSUPPORTED;
   if (num_routes < 0) return KF_ERR_INVALID_ARG;
   if (shape->num_seqs == 0) return KF_OK;
+  const bool fp8 = shape->kv_dtype == KF_KV_FP8_E4M3;
   if (!k_pool || !v_pool || !k_new || !v_new || !tail_route || !err_flags ||
       (num_routes > 0 && !routes) || (shape->num_page_ids > 0 && !page_ids))
     return KF_ERR_INVALID_ARG;
-  const void* ptrs[] = {k_pool, v_pool, k_new, v_new, routes, tail_route, page_ids, err_flags};
+  if (fp8 && (!k_scale || !v_scale)) return KF_ERR_INVALID_ARG;
+  const void* ptrs[] = {k_pool, v_pool, k_scale, v_scale, k_new, v_new,
+                        routes, tail_route, page_ids, err_flags};
   for (const void* p : ptrs)
     if (p && !aligned(p, 4)) return KF_ERR_INVALID_ARG;
   kf::AppendArgs a;
   a.k_pool = k_pool;
   a.v_pool = v_pool;
+  a.k_scale = k_scale;
+  a.v_scale = v_scale;
   a.k_new = static_cast<const uint16_t*>(k_new);
   a.v_new = static_cast<const uint16_t*>(v_new);
   a.routes = routes;
@@ -135,7 +139,7 @@ int kf_kv_append(const kf_shape* shape, void* k_pool, void* v_pool, const void* 
   a.num_routes = num_routes;
   a.num_pages = shape->num_pages;
   a.num_page_ids = shape->num_page_ids;
-  return kf::launch_append(a, as_stream(stream)) == hipSuccess ? KF_OK : KF_ERR_HIP;
+  return kf::launch_append(a, fp8, as_stream(stream)) == hipSuccess ? KF_OK : KF_ERR_HIP;
 }
 
 size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes,

@@ -20,6 +20,8 @@ constexpr int kMinSplitPages = 16;    // smallest page range a split workgroup g
 struct AppendArgs {
   void* k_pool;
   void* v_pool;
+  float* k_scale;  // fp8 pools: [num_pages][Hkv]
+  float* v_scale;
   const uint16_t* k_new;
   const uint16_t* v_new;
   kf_route* routes;
@@ -77,7 +79,7 @@ ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_page
 WorkspaceLayout workspace_layout(int32_t num_routes, int32_t num_kv_heads, int32_t group,
                                  int32_t max_chunks);
 
-hipError_t launch_append(const AppendArgs& a, hipStream_t stream);
+hipError_t launch_append(const AppendArgs& a, bool fp8, hipStream_t stream);
 hipError_t launch_partial(const PartialArgs& a, bool fp8, hipStream_t stream);
 hipError_t launch_merge(const MergeArgs& a, hipStream_t stream);
 

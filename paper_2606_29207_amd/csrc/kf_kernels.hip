@@ -92,6 +92,33 @@ __device__ __forceinline__ u32x4 ld16_stream(const T* p) {
 }
 
 // ------------------------------------------------------------------- append
+// float32 -> E4M3FN code, round to nearest even, clamped to +-448 (finite
+// input); the sign bit is the input's.  Normal range: the 3 leading mantissa
+// bits rounded at bit 20 (a carry moves into the exponent); below 2^-6 the
+// grid is uniform with step 2^-9.
+__device__ __forceinline__ uint32_t e4m3_rne(float v) {
+  const uint32_t sign = (__builtin_bit_cast(uint32_t, v) >> 24) & 0x80u;
+  const float a = fminf(fabsf(v), 448.0f);
+  uint32_t code;
+  if (a < 0.015625f) {
+    code = (uint32_t)__builtin_rintf(a * 512.0f);
+  } else {
+    const uint32_t ab = __builtin_bit_cast(uint32_t, a);
+    const uint32_t man = ab & 0x7FFFFFu;
+    const uint32_t rounded = man + 0x7FFFFu + ((man >> 20) & 1u);
+    code = ((((ab >> 23) & 0xFFu) - 120u) << 3) + (rounded >> 20);
+  }
+  return sign | code;
+}
+
+// E4M3FN code -> float32 (exact; the code widens to bf16, then to fp32).
+__device__ __forceinline__ float e4m3_value(uint32_t code) {
+  const uint32_t b2 = __builtin_bit_cast(uint32_t,
+                                         __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(code, 1.0f, false));
+  return __builtin_bit_cast(float, b2 << 16);
+}
+
+template <bool FP8>
 __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
   const int b = blockIdx.x;
   const int r = a.tail_route[b];
@@ -121,15 +148,63 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
   }
   const int slot = (te - tb) % kPage;
   const int H = a.num_kv_heads;
-  uint16_t* kp = static_cast<uint16_t*>(a.k_pool);
-  uint16_t* vp = static_cast<uint16_t*>(a.v_pool);
-  for (int e = threadIdx.x; e < H * kDim; e += blockDim.x) {
-    const int g = e / kDim, d = e % kDim;
-    const size_t head = (size_t)pid * H + g;
-    const uint16_t kv = a.k_new[((size_t)b * H + g) * kDim + d];
-    const uint16_t vv = a.v_new[((size_t)b * H + g) * kDim + d];
-    kp[(head * kPage + slot) * kDim + d] = kv;
-    vp[(head * kDim + d) * kPage + slot] = vv;
+  if constexpr (!FP8) {
+    uint16_t* kp = static_cast<uint16_t*>(a.k_pool);
+    uint16_t* vp = static_cast<uint16_t*>(a.v_pool);
+    for (int e = threadIdx.x; e < H * kDim; e += blockDim.x) {
+      const int g = e / kDim, d = e % kDim;
+      const size_t head = (size_t)pid * H + g;
+      const uint16_t kv = a.k_new[((size_t)b * H + g) * kDim + d];
+      const uint16_t vv = a.v_new[((size_t)b * H + g) * kDim + d];
+      kp[(head * kPage + slot) * kDim + d] = kv;
+      vp[(head * kDim + d) * kPage + slot] = vv;
+    }
+  } else {
+    // One wave per (KV head, K|V); lane l holds dims 2l, 2l+1.  Page scales
+    // follow the E4M3 append rule: the first token of a page sets
+    // scale = amax/28 (16x headroom below 448); a later token with
+    // amax > 448*scale re-encodes the page's earlier slots to amax/28 first;
+    // the token is stored as RNE(x/scale).  All arithmetic in float32.
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    const int d0 = 2 * lane;
+    for (int pr = w; pr < 2 * H; pr += nw) {
+      const int g = pr >> 1;
+      const bool is_v = pr & 1;
+      const uint16_t* src = (is_v ? a.v_new : a.k_new) + ((size_t)b * H + g) * kDim + d0;
+      const float x0 = __builtin_bit_cast(float, (uint32_t)src[0] << 16);
+      const float x1 = __builtin_bit_cast(float, (uint32_t)src[1] << 16);
+      float amax = fmaxf(fabsf(x0), fabsf(x1));
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) amax = fmaxf(amax, __shfl_xor(amax, m));
+      float* scales = is_v ? a.v_scale : a.k_scale;
+      uint8_t* page = static_cast<uint8_t*>(is_v ? a.v_pool : a.k_pool) +
+                      ((size_t)pid * H + g) * (kPage * kDim);
+      // element (slot s, dim d): K page [s][d], V page [d][s]
+      auto at = [&](int s_, int d_) -> uint8_t* {
+        return page + (is_v ? d_ * kPage + s_ : s_ * kDim + d_);
+      };
+      float scale;
+      if (slot == 0) {
+        scale = amax > 0.0f ? amax / 28.0f : 1.0f;
+      } else {
+        scale = scales[(size_t)pid * H + g];
+        if (amax > 448.0f * scale) {
+          const float fresh = amax / 28.0f;
+          for (int s_ = 0; s_ < slot; ++s_) {
+            uint8_t* p0 = at(s_, d0);
+            uint8_t* p1 = at(s_, d0 + 1);
+            const float v0 = e4m3_value(*p0) * scale;
+            const float v1 = e4m3_value(*p1) * scale;
+            *p0 = (uint8_t)e4m3_rne(v0 / fresh);
+            *p1 = (uint8_t)e4m3_rne(v1 / fresh);
+          }
+          scale = fresh;
+        }
+      }
+      if (lane == 0) scales[(size_t)pid * H + g] = scale;
+      *at(slot, d0) = (uint8_t)e4m3_rne(x0 / scale);
+      *at(slot, d0 + 1) = (uint8_t)e4m3_rne(x1 / scale);
+    }
   }
   __syncthreads();  // every thread has read tok_end before it moves
   if (threadIdx.x == 0) a.routes[r].tok_end = te + 1;
@@ -600,9 +675,12 @@ __global__ __launch_bounds__(64) void merge_kernel(MergeArgs a) {
 
 }  // namespace
 
-hipError_t launch_append(const AppendArgs& a, hipStream_t stream) {
+hipError_t launch_append(const AppendArgs& a, bool fp8, hipStream_t stream) {
   if (a.num_seqs == 0) return hipSuccess;
-  hipLaunchKernelGGL(append_kernel, dim3(a.num_seqs), dim3(256), 0, stream, a);
+  if (fp8)
+    hipLaunchKernelGGL(append_kernel<true>, dim3(a.num_seqs), dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL(append_kernel<false>, dim3(a.num_seqs), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

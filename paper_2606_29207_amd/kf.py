@@ -60,7 +60,7 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib = ctypes.CDLL(path)
     vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
     sp = ctypes.POINTER(Shape)
-    lib.kf_kv_append.argtypes = [sp, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp]
+    lib.kf_kv_append.argtypes = [sp, vp, vp, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp]
     lib.kf_kv_append.restype = ctypes.c_int
     lib.kf_partial_attn_workspace_bytes.argtypes = [sp, i32, i32]
     lib.kf_partial_attn_workspace_bytes.restype = sz
@@ -147,8 +147,9 @@ def shape_of(q, k_pool, page_ids, scale) -> Shape:
 
 
 def kv_append(shape: Shape, k_pool, v_pool, k_new, v_new, routes, tail_route, page_ids,
-              err_flags, stream=None):
-    """kf_kv_append.  routes: int32 [R, 6] (updated in place)."""
+              err_flags, stream=None, k_scale=None, v_scale=None):
+    """kf_kv_append.  routes: int32 [R, 6] (updated in place); fp8 pools also
+    take (and update) k_scale/v_scale float32 [P, Hkv]."""
     lib = load()
     for t, n in ((k_pool, "k_pool"), (v_pool, "v_pool"), (k_new, "k_new"), (v_new, "v_new"),
                  (routes, "routes"), (tail_route, "tail_route"), (page_ids, "page_ids"),
@@ -160,9 +161,15 @@ def kv_append(shape: Shape, k_pool, v_pool, k_new, v_new, routes, tail_route, pa
     _need(k_new.element_size() == 2 and v_new.element_size() == 2, "k_new/v_new must be bf16")
     _need(tail_route.numel() >= B and tail_route.dtype == torch.int32, "tail_route: int32 [num_seqs]")
     _check_tables(shape, k_pool, v_pool, routes, page_ids)
-    st = lib.kf_kv_append(ctypes.byref(shape), _ptr(k_pool), _ptr(v_pool), _ptr(k_new),
-                          _ptr(v_new), _ptr(routes), routes.shape[0], _ptr(tail_route),
-                          _ptr(page_ids), _ptr(err_flags), _stream(stream))
+    if shape.kv_dtype == KV_FP8_E4M3:
+        for t, n in ((k_scale, "k_scale"), (v_scale, "v_scale")):
+            _need(t is not None, f"{n} is required for fp8 pools")
+            _dev(t, n)
+            _need(t.dtype == torch.float32 and t.numel() >= shape.num_pages * shape.num_kv_heads,
+                  f"{n} must be float32 [num_pages, num_kv_heads]")
+    st = lib.kf_kv_append(ctypes.byref(shape), _ptr(k_pool), _ptr(v_pool), _ptr(k_scale),
+                          _ptr(v_scale), _ptr(k_new), _ptr(v_new), _ptr(routes), routes.shape[0],
+                          _ptr(tail_route), _ptr(page_ids), _ptr(err_flags), _stream(stream))
     _check(st, "kf_kv_append")
 
 

@@ -72,7 +72,8 @@ class DecodeState:
     # ---------------------------------------------------------------- calls
     def append(self, k_new: torch.Tensor, v_new: torch.Tensor, stream=None):
         kf.kv_append(self.shape, self.k_pool, self.v_pool, k_new, v_new, self.routes,
-                     self.tail_route, self.page_ids, self.err_flags, stream)
+                     self.tail_route, self.page_ids, self.err_flags, stream,
+                     self.k_scale, self.v_scale)
 
     def partial(self, stream=None):
         kf.partial_attn(self.shape, self.q, self.k_pool, self.v_pool, self.routes,

@@ -12,29 +12,37 @@ O_REL_L2 = 1e-3
 LSE_MAX_ABS = 1e-4
 
 
-def run_oracle(inst, steps=1, tail_route=None):
+def run_oracle(inst, steps=1, tail_route=None, new_tokens=None):
     """Oracle decode: per step append (if the workload appends), then
-    partials of every route, then the merge.  Returns the final state."""
+    partials of every route, then the merge.  Returns the final state.
+    ``new_tokens(step)`` replaces the instance's token stream."""
     wl = inst.wl
+    new_tokens = new_tokens or inst.new_tokens
     kp, vp, routes = inst.k_pool, inst.v_pool, inst.routes.copy()
+    ks, vs = inst.k_scale, inst.v_scale
     tail = inst.tail_route if tail_route is None else tail_route
     flags = 0
     for s in range(steps):
         if wl.appends:
-            kn, vn = inst.new_tokens(s)
-            kp, vp, routes, f = oracle.kv_append(kp, vp, routes, inst.page_ids, tail, kn, vn)
+            kn, vn = new_tokens(s)
+            if ks is None:
+                kp, vp, routes, f = oracle.kv_append(kp, vp, routes, inst.page_ids, tail, kn, vn)
+            else:
+                kp, vp, ks, vs, routes, f = oracle.kv_append(kp, vp, routes, inst.page_ids, tail,
+                                                             kn, vn, ks, vs)
             flags |= f
     o_part, lse_part, f1 = oracle.partial_attn(
         inst.q, kp, vp, routes, inst.page_ids, num_kv_heads=wl.num_kv_heads, scale=inst.scale,
-        max_pages_per_route=inst.max_pages_per_route, k_scale=inst.k_scale, v_scale=inst.v_scale)
+        max_pages_per_route=inst.max_pages_per_route, k_scale=ks, v_scale=vs)
     out, lse, f2 = oracle.merge_partials(o_part, lse_part, inst.seq_route_begin)
-    return dict(k_pool=kp, v_pool=vp, routes=routes, o_part=o_part, lse_part=lse_part,
-                out=out, lse=lse, flags=flags | f1 | f2)
+    return dict(k_pool=kp, v_pool=vp, k_scale=ks, v_scale=vs, routes=routes, o_part=o_part,
+                lse_part=lse_part, out=out, lse=lse, flags=flags | f1 | f2)
 
 
-def run_gpu(inst, steps=1, tail_route=None, nan_fill=True):
+def run_gpu(inst, steps=1, tail_route=None, nan_fill=True, new_tokens=None):
     """HIP path: the same sequence of calls through the C ABI."""
     import torch
+    new_tokens = new_tokens or inst.new_tokens
     from paper_2606_29207_amd.step import DecodeState
     st = DecodeState.from_instance(inst)
     if tail_route is not None:
@@ -44,7 +52,7 @@ def run_gpu(inst, steps=1, tail_route=None, nan_fill=True):
             for t in (st.o_part, st.lse_part, st.out, st.lse):
                 t.fill_(float("nan"))
         if inst.wl.appends:
-            kn, vn = st.upload_new_tokens(*inst.new_tokens(s))
+            kn, vn = st.upload_new_tokens(*new_tokens(s))
             st.step(kn, vn)
         else:
             st.step()
@@ -61,7 +69,9 @@ def host(st):
         vp = vp.view(torch.int16).numpy().view(np.uint16)
     else:
         kp, vp = kp.view(torch.uint8).numpy(), vp.view(torch.uint8).numpy()
-    return dict(k_pool=kp, v_pool=vp, routes=st.routes.cpu().numpy(),
+    ks = None if st.k_scale is None else st.k_scale.cpu().numpy()
+    vs = None if st.v_scale is None else st.v_scale.cpu().numpy()
+    return dict(k_pool=kp, v_pool=vp, k_scale=ks, v_scale=vs, routes=st.routes.cpu().numpy(),
                 o_part=st.o_part.cpu().numpy().astype(np.float64),
                 lse_part=st.lse_part.cpu().numpy().astype(np.float64),
                 out=st.out.cpu().numpy().astype(np.float64),
@@ -103,6 +113,9 @@ def compare_all(g, o, pools=True):
         assert np.array_equal(g["routes"], o["routes"]), "routes differ"
         assert np.array_equal(g["k_pool"], o["k_pool"]), "K pool differs"
         assert np.array_equal(g["v_pool"], o["v_pool"]), "V pool differs"
+        if o.get("k_scale") is not None:
+            assert np.array_equal(g["k_scale"], o["k_scale"]), "K scales differ"
+            assert np.array_equal(g["v_scale"], o["v_scale"]), "V scales differ"
     assert g["flags"] == o["flags"], f"flags {g['flags']} != {o['flags']}"
     assert_close_o(g["o_part"], o["o_part"], "o_part")
     assert_close_lse(g["lse_part"], o["lse_part"], "lse_part")

@@ -114,16 +114,15 @@ def test_partial_attn_zero_routes_is_a_no_op(lib):
 
 def test_append_host_checks(lib):
     v = ctypes.c_void_p
+    rest = [v(FAKE), v(FAKE), v(FAKE), 4, v(FAKE), v(FAKE), v(FAKE), None]   # k_new .. stream
     s = _shape(kv_dtype=kf.KV_FP8_E4M3)
-    args = [v(FAKE)] * 4 + [v(FAKE), 4, v(FAKE), v(FAKE), v(FAKE), None]
-    assert lib.kf_kv_append(ctypes.byref(s), *args) == -2          # fp8 append unsupported
+    assert lib.kf_kv_append(ctypes.byref(s), v(FAKE), v(FAKE), None, None, *rest) == -1   # fp8 w/o scales
     s = _shape()
-    bad = [v(FAKE), None] + [v(FAKE)] * 2 + [v(FAKE), 4, v(FAKE), v(FAKE), v(FAKE), None]
-    assert lib.kf_kv_append(ctypes.byref(s), *bad) == -1          # null v_pool
-    bad = [v(FAKE)] * 4 + [v(FAKE), 4, v(FAKE + 1), v(FAKE), v(FAKE), None]
-    assert lib.kf_kv_append(ctypes.byref(s), *bad) == -1          # misaligned tail_route
+    assert lib.kf_kv_append(ctypes.byref(s), v(FAKE), None, None, None, *rest) == -1       # null v_pool
+    bad = [v(FAKE), v(FAKE), v(FAKE), 4, v(FAKE + 1), v(FAKE), v(FAKE), None]
+    assert lib.kf_kv_append(ctypes.byref(s), v(FAKE), v(FAKE), None, None, *bad) == -1    # misaligned tail
     s0 = _shape(num_seqs=0)
-    assert lib.kf_kv_append(ctypes.byref(s0), *([None] * 4 + [None, 0, None, None, None, None])) == 0
+    assert lib.kf_kv_append(ctypes.byref(s0), *([None] * 6), None, 0, None, None, None, None) == 0
 
 
 def test_merge_host_checks(lib):

@@ -14,7 +14,7 @@ import pytest
 
 import oracle
 from kf_testlib import compare_all, host, run_gpu, run_oracle, assert_close_o, assert_close_lse
-from kf_workloads import make_instance, workload
+from kf_workloads import bf16_bits_to_f32, f32_to_bf16_bits, make_instance, workload
 
 pytestmark = [pytest.mark.gpu, pytest.mark.filterwarnings("ignore::RuntimeWarning")]
 
@@ -28,6 +28,9 @@ CASES = {
     "agentic_small": ("agentic_mix", dict(num_seqs=6, ctx_range=(100, 6000), part_tokens=2048), None, 2),
     "million_small": ("million_ctx", dict(num_seqs=2, part_tokens=4096), [20000, 20000], 1),
     "wide_fp8_small": ("wide_gqa_fp8", dict(num_seqs=3, part_tokens=1024), [3000, 2048, 1111], 1),
+    # E4M3 tail append across page boundaries (new pages, re-encoded pages)
+    "fp8_append": ("wide_gqa_fp8", dict(num_seqs=3, part_tokens=1024, appends=1),
+                   [3000, 2048, 1111], 20),
     "mha_g1": ("llama8b_32k", dict(num_seqs=2, num_q_heads=8, num_kv_heads=8, part_tokens=512), [900, 77], 1),
     "g16": ("llama8b_32k", dict(num_seqs=2, num_q_heads=32, num_kv_heads=2, part_tokens=1000), [1500, 2100], 1),
     "g8_bf16": ("llama8b_32k", dict(num_seqs=2, num_q_heads=64, num_kv_heads=8, part_tokens=700), [1400, 333], 1),
@@ -60,6 +63,38 @@ def test_fp8_second_seed(gpu):
     inst = make_instance(workload("wide_gqa_fp8", num_seqs=2, part_tokens=2048),
                          seed=2, seq_lens=[4500, 1234])
     compare_all(host(run_gpu(inst, 1)), run_oracle(inst, 1))
+
+
+def test_fp8_append_reencodes_pages_begun_by_appends():
+    """E4M3 append with one step's tokens 100x larger than the rest: pages
+    begun by earlier appends of that step's tails are re-encoded to the new
+    scale; codes and scales bit-exact, attention within tolerance."""
+    wl = workload("wide_gqa_fp8", num_seqs=3, part_tokens=1024, appends=1)
+    inst = make_instance(wl, seed=5, steps=24, seq_lens=[3000, 2048, 1111])
+
+    def tokens(s):
+        kn, vn = inst.new_tokens(s)
+        if s != 12:
+            return kn, vn
+        up = lambda t: f32_to_bf16_bits(bf16_bits_to_f32(t) * np.float32(100.0))
+        return up(kn), up(vn)
+
+    o = run_oracle(inst, steps=24, new_tokens=tokens)
+    g = host(run_gpu(inst, steps=24, new_tokens=tokens))
+    for key in ("routes", "k_pool", "v_pool", "k_scale", "v_scale"):
+        assert np.array_equal(g[key], o[key]), f"{key} differs"
+    assert g["flags"] == o["flags"] == 0
+    # the inputs are scaled up 100x, so the float32 error budget is too
+    for key in ("o_part", "out"):
+        ref = o[key][np.isfinite(o[key])]
+        tol = 2e-3 * max(1.0, float(np.abs(ref).max()))
+        assert np.array_equal(np.isnan(g[key]), np.isnan(o[key]))
+        assert float(np.abs(g[key] - o[key])[np.isfinite(o[key])].max()) <= tol, key
+    for key in ("lse_part", "lse"):
+        fin = np.isfinite(o[key])
+        assert np.array_equal(fin, np.isfinite(g[key]))
+        tol = 1e-4 * max(1.0, float(np.abs(o[key][fin]).max()))
+        assert float(np.abs(g[key] - o[key])[fin].max()) <= tol, key
 
 
 def test_empty_tail_route_then_append(gpu):

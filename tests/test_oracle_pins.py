@@ -494,3 +494,140 @@ def test_unmutated_pipeline_is_exact():
 ], ids=lambda kw: next(iter(kw.values())).__name__)
 def test_planted_mistake_is_caught(kw):
     assert _pipeline_error(**kw) > 1e-3
+
+
+# ------------------------------------------------------------- fp8 append
+def test_e4m3_encode_matches_torch_cast():
+    """Nearest-even encoding onto the E4M3FN grid equals torch's float8_e4m3fn
+    cast (on values clamped to +-448), including ties, subnormals and -0."""
+    rng = np.random.default_rng(21)
+    x = np.concatenate([rng.normal(size=5000).astype(np.float32) * s
+                        for s in (1e-3, 0.05, 1, 30, 200, 1000)])
+    grid = oracle.e4m3_table()[:0x7F]
+    mids = ((grid[:-1] + grid[1:]) / 2).astype(np.float32)
+    x = np.concatenate([x, mids, -mids, np.float32([0.0, -0.0, 448, -448, 464, 1e6, 2.0 ** -12])])
+    ref = torch.from_numpy(np.clip(x, -448, 448)).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    np.testing.assert_array_equal(oracle.e4m3_encode_rne(x), ref)
+
+
+def _fp8_append_run(steps, kv_append=None, big=None):
+    """Appends into an E4M3 pool; ``big`` = (step, factor) scales one step's
+    new tokens up so that their pages must be re-encoded."""
+    wl = workload("wide_gqa_fp8", num_seqs=2, num_q_heads=16, num_kv_heads=2, part_tokens=64,
+                  appends=1)
+    inst = make_instance(wl, seed=22, steps=steps, seq_lens=[70, 45])
+    kv_append = kv_append or oracle.kv_append
+    kp, vp, ks, vs, routes = inst.k_pool, inst.v_pool, inst.k_scale, inst.v_scale, inst.routes
+    written = []               # (step, b, local index j, k bits, v bits, k scales, v scales)
+    for s in range(steps):
+        if big is not None and s == big[0]:
+            inst.before_big = tuple(a.copy() for a in (kp, vp, ks, vs, routes))
+        kn, vn = inst.new_tokens(s)
+        if big is not None and s == big[0]:
+            kn = f32_to_bf16_bits(oracle.bf16_to_f64(kn).astype(np.float32) * big[1])
+            vn = f32_to_bf16_bits(oracle.bf16_to_f64(vn).astype(np.float32) * big[1])
+        for b in range(2):
+            r = inst.tail_route[b]
+            written.append((s, b, int(routes[r, 3] - routes[r, 2]), kn[b], vn[b]))
+        kp, vp, ks, vs, routes, f = kv_append(kp, vp, routes, inst.page_ids, inst.tail_route,
+                                              kn, vn, ks, vs)
+        assert f == 0
+        for i in range(len(written) - 2, len(written)):       # page scales right after the write
+            s_, b, j, kb, vb = written[i][:5]
+            pid = inst.page_ids[int(routes[inst.tail_route[b], 4]) + j // 16]
+            written[i] = (s_, b, j, kb, vb, ks[pid].copy(), vs[pid].copy())
+    return inst, kp, vp, ks, vs, routes, written
+
+
+def _stored(inst, routes, pool, b, j, g, kmajor):
+    r = inst.tail_route[b]
+    pid = inst.page_ids[int(routes[r, 4]) + j // 16]
+    return pid, (pool[pid, g][j % 16, :] if kmajor else pool[pid, g][:, j % 16])
+
+
+def _torch_e4m3(x):
+    return torch.from_numpy(np.clip(np.asarray(x, np.float32), -448, 448)).to(
+        torch.float8_e4m3fn).view(torch.uint8).numpy()
+
+
+def test_fp8_append_first_token_scale_and_codes():
+    """E4M3 append rule on N(0,1) tokens: a page begun by an append has
+    scale = amax(first token)/28 in float32 and is never re-encoded; every
+    token whose page scale has not changed since it was written equals
+    torch's float8_e4m3fn cast of x/scale, so it lies within half an E4M3 step
+    of its bf16 value."""
+    inst, kp, vp, ks, vs, routes, written = _fp8_append_run(40)
+    checked = 0
+    for s_, b, j, kb, vb, ks_then, vs_then in written:
+        for pool, scl, then, bits, kmajor in ((kp, ks, ks_then, kb, True), (vp, vs, vs_then, vb, False)):
+            for g in range(2):
+                pid, codes = _stored(inst, routes, pool, b, j, g, kmajor)
+                x = oracle.bf16_to_f64(bits[g]).astype(np.float32)
+                first = [w for w in written if w[1] == b and w[2] == j - j % 16]
+                if first:                                  # page begun by an append
+                    fx = oracle.bf16_to_f64((first[0][3] if kmajor else first[0][4])[g])
+                    assert scl[pid, g] == np.float32(np.float32(np.abs(fx).max()) / np.float32(28.0))
+                if then[g] != scl[pid, g]:                 # re-encoded later (prefilled page)
+                    continue
+                checked += 1
+                s32 = np.float32(scl[pid, g])
+                np.testing.assert_array_equal(codes, _torch_e4m3((x / s32).astype(np.float32)))
+                deq = oracle.e4m3_to_f64(codes) * np.float64(s32)
+                assert np.all(np.abs(deq - x) <= 2.0 ** -4 * np.abs(x) + np.float64(s32) * 2.0 ** -10)
+    assert checked >= 0.9 * 4 * len(written)
+
+
+def test_fp8_append_reencodes_page_for_large_token():
+    """A token 100x larger than its page's first token: the page's earlier
+    slots are re-encoded to scale' = amax/28 (torch's cast of
+    decode(code)*scale/scale'), and every value stays within two E4M3
+    roundings of its bf16 value."""
+    steps, at = 12, 5                  # tail of b=1 starts a page at j=48 (step 3)
+    inst, kp, vp, ks, vs, routes, written = _fp8_append_run(steps, big=(at, 100.0))
+    kp0, vp0, ks0, vs0, routes0 = inst.before_big
+    b = 1
+    j_big = [w[2] for w in written if w[0] == at and w[1] == b][0]
+    assert j_big % 16 > 0
+    for pool0, sc0, pool, sc, kmajor, idx in ((kp0, ks0, kp, ks, True, 3), (vp0, vs0, vp, vs, False, 4)):
+        for g in range(2):
+            pid, _ = _stored(inst, routes, pool, b, j_big, g, kmajor)
+            big = oracle.bf16_to_f64(written[[i for i, w in enumerate(written)
+                                              if w[0] == at and w[1] == b][0]][idx][g])
+            new_scale = np.float32(np.float32(np.abs(big).max()) / np.float32(28.0))
+            assert sc[pid, g] == new_scale
+            for jj in range(j_big - j_big % 16, j_big):
+                _, old_codes = _stored(inst, routes0, pool0, b, jj, g, kmajor)
+                vals = (oracle.e4m3_to_f64(old_codes).astype(np.float32) * np.float32(sc0[pid, g]))
+                expect = _torch_e4m3((vals.astype(np.float32) / new_scale).astype(np.float32))
+                _, codes = _stored(inst, routes, pool, b, jj, g, kmajor)
+                np.testing.assert_array_equal(codes, expect)
+    for s_, b_, j, kb, vb, _, _ in written:
+        for pool, scl, bits, kmajor in ((kp, ks, kb, True), (vp, vs, vb, False)):
+            for g in range(2):
+                pid, codes = _stored(inst, routes, pool, b_, j, g, kmajor)
+                x = oracle.bf16_to_f64(bits[g])
+                deq = oracle.e4m3_to_f64(codes) * np.float64(scl[pid, g])
+                bound = (2.0 ** -3 + 2.0 ** -8) * np.abs(x) + np.float64(scl[pid, g]) * 2.0 ** -9
+                assert np.all(np.abs(deq - x) <= bound)
+
+
+def test_fp8_append_without_reencode_is_caught():
+    """Planted mistake: never re-encode a page when a larger token arrives
+    (that token then saturates at 448*scale); the re-encode pin must fail."""
+    saved = kf_oracle._append_e4m3
+
+    def no_reencode(page, scales, pid, g, slot, x_bits, kmajor):
+        if slot == 0:
+            return saved(page, scales, pid, g, slot, x_bits, kmajor)
+        x = (np.asarray(x_bits, np.uint16).astype(np.uint32) << 16).view(np.float32)
+        codes = oracle.e4m3_encode_rne((x / np.float32(scales[pid, g])).astype(np.float32))
+        if kmajor:
+            page[slot, :] = codes
+        else:
+            page[:, slot] = codes
+    kf_oracle._append_e4m3 = no_reencode
+    try:
+        with pytest.raises(AssertionError):
+            test_fp8_append_reencodes_page_for_large_token()
+    finally:
+        kf_oracle._append_e4m3 = saved
