@@ -10,6 +10,9 @@ the tail append (Section 3.2, step 3; Section 5.1), local attention over one
 token range producing a partial (Section 3.2, step 3), and the log-sum-exp
 merge of partials (Section 3.2, step 4; Section 5.1).  All functions are
 pinned by tests in ``tests/test_oracle_pins.py``; none is "parity unpinned".
+
+``oracle.kf_policy`` is the attention-node scaling policy (Section 4.2:
+Algorithm 1, Eqs. (1) and (2)), pinned by ``tests/test_policy_pins.py``.
 """
 from .kf_oracle import (  # noqa: F401
     EFLAG_TAIL_FULL,
