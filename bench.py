@@ -35,7 +35,7 @@ sys.path.insert(0, ROOT)
 METRIC = "achieved HBM GB/s + µs/step for partial decode attn+merge (Llama-3.1-8B layer)"
 HBM_PEAK_GBPS = 8000.0            # MI355X HBM3E, vendor figure
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_29207_amd", "csrc", "kf_kernels.hip")
-COUNTERS = os.path.join(ROOT, "profiles", "partial_kernel_llama8b_32k_counters.md")
+COUNTERS = os.path.join(ROOT, "profiles", "partial_kernel_{workload}_counters.md")
 
 
 # ---------------------------------------------------------------- bytes model
@@ -124,12 +124,14 @@ def kernel_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def counter_traffic():
+def counter_traffic(workload_name: str, seed: int):
     """Per-launch HBM bytes of the partial kernel from the committed rocprofv3
-    counter summary, or None when it is absent or the kernel has changed."""
-    if not os.path.exists(COUNTERS):
+    counter summary of this workload (seed 1), or None when there is none or
+    the kernel has changed since it was taken."""
+    path = COUNTERS.format(workload=workload_name)
+    if seed != 1 or not os.path.exists(path):
         return None
-    txt = open(COUNTERS).read()
+    txt = open(path).read()
     m = re.search(r"kernel_sha256_16:\s*([0-9a-f]+)", txt)
     t = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", txt)
     if not m or not t or m.group(1) != kernel_hash():
@@ -153,6 +155,43 @@ def calibrate_copy(mib: int):
     dt = time.perf_counter() - t0
     print(json.dumps({"copy_bytes_each_way": n, "seconds": dt, "GBps_rw": 2 * n / dt / 1e9}),
           flush=True)
+
+
+def policy_report(inst, wl, bw_gbps: float, attn_us: float, hbm_bytes: int) -> dict:
+    """Scaling-policy calculator (Section 4.2: Algorithm 1, Eqs. (1), (2)) fed
+    with this run's measured partial-attention bandwidth, for this batch at
+    the full model's depth, through the library's host entry points."""
+    from paper_2606_29207_amd import policy as pol
+    layers = 80 if wl.num_q_heads == 64 else 32          # 70B-like wide GQA, else Llama-3.1-8B
+    t_slo = 0.080 if layers == 80 else 0.050              # the paper's TPOT targets for 70B / 8B
+    t_a_max = pol.layer_budget(t_slo, 0.0, layers, 0.0)
+    p = pol.params(num_kv_heads=wl.num_kv_heads, head_dim=wl.head_dim, num_layers=layers,
+                   elem_bytes=2 if wl.kv_dtype == "bf16" else 1, beta_mem=0.9, beta_slo=0.8,
+                   gamma=0.9, t_a_max=t_a_max, bw_hbm=bw_gbps * 1e9, c_kv_cap=float(hbm_bytes),
+                   t_step=layers * attn_us * 1e-6, t_prewarm=1.0)
+    c, c_mem, c_slo = pol.threshold(p)
+    lens = np.asarray(inst.seq_lens, np.int64)
+    B = len(lens)
+    st = pol.init(p, lens, max_events=4 * B + 8)
+    st.nodes = np.concatenate([st.nodes, np.zeros(B + 1, pol.NODE_DT)])
+    st.ranges = np.concatenate([st.ranges, np.zeros(B + 1, pol.RANGE_DT)])
+    act = np.ones(B, np.uint8)
+    pol.monitor(p, 0, st, act, lens)
+    taus = st.nodes["tau_fill"][:st.num_nodes]
+    tau = float(np.nanmin(taus)) if np.isfinite(taus).any() else None
+    pol.monitor(p, 1, st, act, lens)          # a first pass may spawn; the next ones do not
+    mon_us = pol.time_monitor(p, st, act, lens) * 1e6
+    return {"model_layers": layers, "t_slo_ms": t_slo * 1e3, "t_a_max_us": round(t_a_max * 1e6, 2),
+            "bw_hbm_GBps": round(bw_gbps, 2), "c_kv_cap_GB": round(hbm_bytes / 1e9, 2),
+            "c_mem_GB": round(c_mem / 1e9, 2), "c_slo_GB": round(c_slo / 1e9, 2),
+            "c_thresh_GB": round(c / 1e9, 2), "binding": "slo" if c_slo < c_mem else "mem",
+            "c_total_GB": round(st.c_total / 1e9, 2), "n_a": st.num_nodes,
+            "node_GB_max": round(float(st.nodes["bytes"][:st.num_nodes].max()) / 1e9, 2),
+            "tau_fill_steps_min": None if tau is None else round(tau, 1),
+            "t_step_ms": round(layers * attn_us * 1e-3, 3),
+            "monitor_us_per_call": round(mon_us, 3),
+            "assumptions": "beta_mem 0.9, beta_slo 0.8, gamma 0.9, no per-token overhead, "
+                           "T_step = layers x measured attention+merge, T_prewarm 1 s"}
 
 
 def main(argv=None):
@@ -264,7 +303,7 @@ def main(argv=None):
     am_b = np.mean([b["partial"] + b["merge"] for b in by])
     us_step = wall / K * 1e6
     achieved = par_b / (t_par.mean() * 1e-6) / 1e9
-    traffic = counter_traffic()
+    traffic = counter_traffic(wl.name, args.seed)
     out = {
         "metric": METRIC,
         "value": round(step_b / (us_step * 1e-6) / 1e9, 2),
@@ -298,6 +337,8 @@ def main(argv=None):
                      "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic, "algorithmic_bytes_per_launch": int(par_b)},
         "cpu_baseline": cpu,
+        "policy": policy_report(inst, wl, achieved, float((t_par + t_mrg).mean()),
+                                torch.cuda.mem_get_info()[1]),
     }
     print(json.dumps(out), flush=True)
     return 0

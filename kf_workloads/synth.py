@@ -223,7 +223,7 @@ def _workers() -> int:
 
 
 def make_instance(wl: Workload, seed: int = 1, *, steps: int = 1,
-                  seq_lens=None, empty_tail: bool = False) -> Instance:
+                  seq_lens=None, empty_tail: bool = False, routing=None) -> Instance:
     """Build one seeded instance of ``wl``.
 
     ``steps``      appends the tail routes must hold room for (if wl.appends).
@@ -231,6 +231,10 @@ def make_instance(wl: Workload, seed: int = 1, *, steps: int = 1,
     ``empty_tail`` additionally open a fresh, empty tail route per sequence
                    (a route published at a token boundary, before its first
                    append).
+    ``routing``    an explicit routing table (routes [R, 6], page_ids,
+                   seq_route_begin [B+1], tail_route [B]) used verbatim
+                   instead of routes of part_tokens; its resident ranges
+                   must tile each sequence's [0, seq_lens[b]).
     """
     B, Hq, Hkv, D = wl.num_seqs, wl.num_q_heads, wl.num_kv_heads, wl.head_dim
     assert Hq % Hkv == 0 and wl.page_size == PAGE and D == HEAD_DIM
@@ -240,31 +244,38 @@ def make_instance(wl: Workload, seed: int = 1, *, steps: int = 1,
         np.stack([_rng(seed, wl.wid, _T_Q, b).standard_normal((Hq, D), dtype=np.float32)
                   for b in range(B)]))
 
-    # ---- routes: contiguous token ranges of part_tokens; the last is the tail
-    grow = steps * wl.appends
-    rows, srb, tails = [], [0], []
-    for b in range(B):
-        n = int(lens[b])
-        starts = list(range(0, n, wl.part_tokens)) or [0]
-        ends = [min(s + wl.part_tokens, n) for s in starts]
-        if empty_tail:
-            starts.append(n)
-            ends.append(n)
-        for k, (s, e) in enumerate(zip(starts, ends)):
-            last = k == len(starts) - 1
-            cap = -(-((e - s) + (grow if last else 0)) // PAGE)
-            rows.append([b, k, s, e, 0, cap])
-        tails.append(len(rows) - 1 if wl.appends or empty_tail else -1)
-        srb.append(len(rows))
-    routes = np.array(rows, dtype=np.int32).reshape(-1, 6)
-    caps = routes[:, 5].astype(np.int64)
-    total = int(caps.sum())
-    routes[:, 4] = np.concatenate([[0], np.cumsum(caps)[:-1]]).astype(np.int32)
-    if wl.permuted:
-        page_ids = _rng(seed, wl.wid, _T_PERM).permutation(total).astype(np.int32)
+    if routing is not None:
+        routes = np.array(routing[0], dtype=np.int32).reshape(-1, 6)
+        page_ids = np.array(routing[1], dtype=np.int32)
+        srb = [int(x) for x in routing[2]]
+        tails = [int(x) for x in routing[3]]
+        P = max(int(page_ids.max()) + 1 if len(page_ids) else 1, 1)
     else:
-        page_ids = np.arange(total, dtype=np.int32)
-    P = max(total, 1)
+        # ---- routes: contiguous token ranges of part_tokens; the last is the tail
+        grow = steps * wl.appends
+        rows, srb, tails = [], [0], []
+        for b in range(B):
+            n = int(lens[b])
+            starts = list(range(0, n, wl.part_tokens)) or [0]
+            ends = [min(s + wl.part_tokens, n) for s in starts]
+            if empty_tail:
+                starts.append(n)
+                ends.append(n)
+            for k, (s, e) in enumerate(zip(starts, ends)):
+                last = k == len(starts) - 1
+                cap = -(-((e - s) + (grow if last else 0)) // PAGE)
+                rows.append([b, k, s, e, 0, cap])
+            tails.append(len(rows) - 1 if wl.appends or empty_tail else -1)
+            srb.append(len(rows))
+        routes = np.array(rows, dtype=np.int32).reshape(-1, 6)
+        caps = routes[:, 5].astype(np.int64)
+        total = int(caps.sum())
+        routes[:, 4] = np.concatenate([[0], np.cumsum(caps)[:-1]]).astype(np.int32)
+        if wl.permuted:
+            page_ids = _rng(seed, wl.wid, _T_PERM).permutation(total).astype(np.int32)
+        else:
+            page_ids = np.arange(total, dtype=np.int32)
+        P = max(total, 1)
 
     fp8 = wl.kv_dtype == "fp8"
     edt = np.uint8 if fp8 else np.uint16

@@ -15,7 +15,7 @@ CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libkf.so")
 ARCH = "gfx950"
 
-SOURCES = ["kf_api.cpp", "kf_kernels.hip"]
+SOURCES = ["kf_api.cpp", "kf_policy.cpp", "kf_kernels.hip"]
 
 # Packed-FP32 VALU instructions are kept out of the device code on purpose.
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

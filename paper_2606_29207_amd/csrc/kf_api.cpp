@@ -100,6 +100,8 @@ const char* kf_status_str(int status) {
     case KF_ERR_UNSUPPORTED: return "unsupported shape or dtype";
     case KF_ERR_WORKSPACE: return "workspace missing or too small";
     case KF_ERR_HIP: return "HIP runtime error";
+    case KF_ERR_CAPACITY: return "output array too small";
+    case KF_ERR_INFEASIBLE: return "infeasible budget";
     default: return "unknown status";
   }
 }

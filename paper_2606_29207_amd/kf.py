@@ -20,6 +20,13 @@ MAX_GROUP = 16
 KV_BF16 = 0
 KV_FP8_E4M3 = 1
 
+ERR_INVALID_ARG = -1
+ERR_UNSUPPORTED = -2
+ERR_WORKSPACE = -3
+ERR_HIP = -4
+ERR_CAPACITY = -5
+ERR_INFEASIBLE = -6
+
 EFLAG_TAIL_FULL = 1
 EFLAG_BAD_ROUTE = 2
 EFLAG_BAD_PAGE = 4

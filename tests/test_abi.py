@@ -7,10 +7,11 @@ import re
 
 import pytest
 
-from paper_2606_29207_amd import kf
+from paper_2606_29207_amd import kf, policy
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "kf.h")
+POLICY_HEADER = os.path.join(ROOT, "include", "kf_policy.h")
 
 FAKE = 0x10000      # non-null, 256-byte aligned stand-in; never dereferenced here
 
@@ -23,18 +24,19 @@ def lib():
     return kf.load()
 
 
-def _declared_functions():
-    src = open(HEADER).read()
+def _declared_functions(header=HEADER):
+    src = open(header).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
     return sorted(set(re.findall(r"\b(kf_[a-z0-9_]+)\s*\(", src)))
 
 
 def test_header_and_binding_agree():
     assert _declared_functions() == sorted(kf.EXPORTS)
+    assert _declared_functions(POLICY_HEADER) == sorted(policy.EXPORTS)
 
 
 def test_library_exports_every_declared_symbol(lib):
-    for name in _declared_functions():
+    for name in _declared_functions() + _declared_functions(POLICY_HEADER):
         assert hasattr(lib, name), name
     assert kf.version().startswith("kf ")
 
@@ -42,11 +44,14 @@ def test_library_exports_every_declared_symbol(lib):
 def test_struct_layouts_match_header():
     assert ctypes.sizeof(kf.Route) == 24
     assert ctypes.sizeof(kf.Shape) == 36
+    assert ctypes.sizeof(policy.Params) == 80
+    assert policy.RANGE_DT.itemsize == 24 and policy.NODE_DT.itemsize == 32
+    assert policy.EVENT_DT.itemsize == 24 and policy.ROUTE_DT.itemsize == 24
 
 
 def test_status_strings(lib):
     for code, text in ((0, "ok"), (-1, "invalid argument"), (-2, "unsupported"),
-                       (-3, "workspace"), (-4, "HIP")):
+                       (-3, "workspace"), (-4, "HIP"), (-5, "too small"), (-6, "infeasible")):
         assert text in kf.status_str(code)
     assert kf.status_str(12345) == "unknown status"
 
