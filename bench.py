@@ -15,7 +15,7 @@ Flags: --gpus N (only 1 is supported: the path runs on one GPU)
        --steps K --warmup W --workload NAME --seed S --no-cpu-baseline
        --calibrate-copy MiB (time a plain device copy instead; for counter
        calibration under rocprofv3)
-       --schedule serial|query_first
+       --schedule fused|serial|query_first (default fused: kf_decode_step)
 """
 from __future__ import annotations
 
@@ -203,10 +203,12 @@ def main(argv=None):
     ap.add_argument("--seed", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB")
-    ap.add_argument("--schedule", choices=("serial", "query_first"), default="serial",
-                    help="serial: append -> partial -> merge on one stream; query_first: "
-                         "historical partials from q alone on one stream, append + tail "
-                         "partials on a second, merge after both")
+    ap.add_argument("--schedule", choices=("fused", "serial", "query_first"), default="fused",
+                    help="fused: kf_decode_step (append fused into the partial-attention "
+                         "launch for bf16 pools, then the merge); serial: append -> partial -> "
+                         "merge as three calls on one stream; query_first: historical partials "
+                         "from q alone on one stream, append + tail partials on a second, merge "
+                         "after both")
     args = ap.parse_args(argv)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -221,7 +223,7 @@ def main(argv=None):
     wl = workload(args.workload)
     K, W = args.steps, args.warmup
     t = time.perf_counter()
-    inst = make_instance(wl, seed=args.seed, steps=W + K)
+    inst = make_instance(wl, seed=args.seed, steps=W + 2 * K)
     print(f"[bench] generated {wl.name} in {time.perf_counter() - t:.1f}s", file=sys.stderr, flush=True)
 
     cpu = None
@@ -235,7 +237,7 @@ def main(argv=None):
     torch.cuda.set_device(0)
     st = DecodeState.from_instance(inst)
     news = [st.upload_new_tokens(*inst.new_tokens(s)) if wl.appends else (None, None)
-            for s in range(W + K)]
+            for s in range(W + 2 * K)]
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
     print(f"[bench] uploaded; warmup {W} steps", file=sys.stderr, flush=True)
@@ -246,34 +248,51 @@ def main(argv=None):
             print("bench.py: --schedule query_first needs a workload that appends", file=sys.stderr)
             return 2
         st.setup_query_first()
-    for s in range(W):
+    fused = args.schedule == "fused" and wl.appends > 0
+
+    def one_step(kv):
         if qf:
-            st.step_query_first(*news[s])
+            st.step_query_first(*kv)
+        elif fused:
+            st.step_fused(*kv)
         else:
-            st.step(*news[s])
+            st.step(*kv)
+
+    for s in range(W):
+        one_step(news[s])
     torch.cuda.synchronize()
 
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    # timed region: K whole steps, nothing recorded between the kernels (an
+    # event marker between two launches lengthens the gap between them)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    for i in range(K):
+        one_step(news[W + i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    # breakdown pass: the next K steps as three calls with HIP events around
+    # each, on the stream the kernels are launched on (the fused schedule
+    # runs the same partial kernel; its launch cannot be bracketed alone)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    torch.cuda.synchronize()
     for i in range(K):
         e = ev[i]
         e[0].record(stream)
         if qf:
-            st.step_query_first(*news[W + i])
+            st.step_query_first(*news[W + K + i])
             e[1].record(stream)
             e[2].record(stream)
             e[3].record(stream)
             continue
         if wl.appends:
-            st.append(*news[W + i])
+            st.append(*news[W + K + i])
         e[1].record(stream)
         st.partial()
         e[2].record(stream)
         st.merge()
         e[3].record(stream)
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
     flags = st.flags()
     if flags:
         print(f"[bench] device error flags {flags}", file=sys.stderr, flush=True)
@@ -299,8 +318,9 @@ def main(argv=None):
     t_mrg = np.array([e[2].elapsed_time(e[3]) for e in ev]) * 1e3
     by = [step_bytes(inst, W + i) for i in range(K)]
     step_b = np.mean([b["append"] + b["partial"] + b["merge"] for b in by])
-    par_b = np.mean([b["partial"] for b in by])
-    am_b = np.mean([b["partial"] + b["merge"] for b in by])
+    by2 = [step_bytes(inst, W + K + i) for i in range(K)]
+    par_b = np.mean([b["partial"] for b in by2])
+    am_b = np.mean([b["partial"] + b["merge"] for b in by2])
     us_step = wall / K * 1e6
     achieved = par_b / (t_par.mean() * 1e-6) / 1e9
     traffic = counter_traffic(wl.name, args.seed)
@@ -323,6 +343,8 @@ def main(argv=None):
                    "context": int(inst.seq_lens.max()), "route_tokens": wl.part_tokens,
                    "routes": int(len(inst.routes)), "page_tokens": 16,
                    "appends_per_step": wl.appends, "kv_dtype": wl.kv_dtype},
+        "schedule": "fused" if fused else "serial",
+        "breakdown_pass": "a second run of K steps as three calls with HIP events around each",
         "breakdown_us": {"append": round(float(t_app.mean()), 2) if wl.appends else None,
                          "partial_attn": round(float(t_par.mean()), 2),
                          "partial_attn_p10_p90": [round(float(np.percentile(t_par, 10)), 2),

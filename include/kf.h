@@ -197,6 +197,27 @@ int kf_merge_partials(int32_t num_seqs, int32_t num_routes, int32_t num_q_heads,
                       const int32_t* seq_route_begin, float* out, float* lse_out,
                       int32_t* err_flags, void* stream);
 
+/*
+ * kf_decode_step -- one whole decode step (Section 3.2, steps 3 and 4;
+ * Section 5.1): the tail append, partial attention of every route and the
+ * merge, with the results, flags and route updates of
+ *   kf_kv_append -> kf_partial_attn -> kf_merge_partials
+ * on the same arguments (each argument as documented there; the workspace
+ * is sized by kf_partial_attn_workspace_bytes).  bf16 pools run it in two
+ * launches instead of three: the workgroup that attends over a tail's last
+ * page first writes the step's token into it and attends over it, and the
+ * merge advances the tails' tok_end and raises the append's flags.  fp8
+ * pools run the three kernels (an append may re-encode a whole page).
+ * All host checks of the three calls are made before anything is launched.
+ */
+int kf_decode_step(const kf_shape* shape, const void* q, void* k_pool, void* v_pool,
+                   float* k_scale, float* v_scale, const void* k_new, const void* v_new,
+                   kf_route* routes, int32_t num_routes, const int32_t* tail_route,
+                   int32_t max_pages_per_route, const int32_t* page_ids,
+                   const int32_t* seq_route_begin, float* o_part, float* lse_part, float* out,
+                   float* lse_out, void* workspace, size_t workspace_bytes, int32_t* err_flags,
+                   void* stream);
+
 /* Static description of a status code (never NULL). */
 const char* kf_status_str(int status);
 

@@ -108,10 +108,23 @@ const char* kf_status_str(int status) {
 
 const char* kf_version(void) { return "kf 0.1 gfx950"; }
 
-int kf_kv_append(const kf_shape* shape, void* k_pool, void* v_pool, float* k_scale,
-                 float* v_scale, const void* k_new, const void* v_new, kf_route* routes,
-                 int32_t num_routes, const int32_t* tail_route, const int32_t* page_ids,
-                 int32_t* err_flags, void* stream) {
+size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes,
+                                       int32_t max_pages_per_route) {
+  if (check_shape(shape) != KF_OK || num_routes < 0 || max_pages_per_route < 0) return 0;
+  const int32_t group = shape->num_q_heads / shape->num_kv_heads;
+  const kf::ChunkPlan plan = kf::plan_chunks(num_routes, shape->num_kv_heads, max_pages_per_route);
+  return kf::workspace_layout(num_routes, shape->num_kv_heads, group, plan.max_chunks).total;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Host checks of kf_kv_append; fills the kernel arguments.
+int prepare_append(const kf_shape* shape, void* k_pool, void* v_pool, float* k_scale,
+                   float* v_scale, const void* k_new, const void* v_new, kf_route* routes,
+                   int32_t num_routes, const int32_t* tail_route, const int32_t* page_ids,
+                   int32_t* err_flags, kf::AppendArgs& a) {
   int st = check_shape(shape);
   if (st != KF_OK) return st;
   if (num_routes < 0) return KF_ERR_INVALID_ARG;
@@ -125,7 +138,6 @@ int kf_kv_append(const kf_shape* shape, void* k_pool, void* v_pool, float* k_sca
                         routes, tail_route, page_ids, err_flags};
   for (const void* p : ptrs)
     if (p && !aligned(p, 4)) return KF_ERR_INVALID_ARG;
-  kf::AppendArgs a;
   a.k_pool = k_pool;
   a.v_pool = v_pool;
   a.k_scale = k_scale;
@@ -141,28 +153,17 @@ int kf_kv_append(const kf_shape* shape, void* k_pool, void* v_pool, float* k_sca
   a.num_routes = num_routes;
   a.num_pages = shape->num_pages;
   a.num_page_ids = shape->num_page_ids;
-  return kf::launch_append(a, fp8, as_stream(stream)) == hipSuccess ? KF_OK : KF_ERR_HIP;
+  return KF_OK;
 }
 
-size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes,
-                                       int32_t max_pages_per_route) {
-  if (check_shape(shape) != KF_OK || num_routes < 0 || max_pages_per_route < 0) return 0;
-  const int32_t group = shape->num_q_heads / shape->num_kv_heads;
-  const kf::ChunkPlan plan = kf::plan_chunks(num_routes, shape->num_kv_heads, max_pages_per_route);
-  return kf::workspace_layout(num_routes, shape->num_kv_heads, group, plan.max_chunks).total;
-}
-
-}  // extern "C"
-
-namespace {
-
-// Shared body of kf_partial_attn and kf_partial_attn_subset.
-int partial_attn_impl(const kf_shape* shape, const void* q, const void* k_pool, const void* v_pool,
-                      const float* k_scale, const float* v_scale, const kf_route* routes,
-                      int32_t num_routes, const int32_t* route_list, int32_t num_launch,
-                      int32_t max_pages_per_route, const int32_t* page_ids, float* o_part,
-                      float* lse_part, void* workspace, size_t workspace_bytes,
-                      int32_t* err_flags, void* stream) {
+// Host checks of kf_partial_attn / kf_partial_attn_subset; fills the kernel
+// arguments (a.num_units_routes == 0: nothing to launch).
+int prepare_partial(const kf_shape* shape, const void* q, const void* k_pool, const void* v_pool,
+                    const float* k_scale, const float* v_scale, const kf_route* routes,
+                    int32_t num_routes, const int32_t* route_list, int32_t num_launch,
+                    int32_t max_pages_per_route, const int32_t* page_ids, float* o_part,
+                    float* lse_part, void* workspace, size_t workspace_bytes, int32_t* err_flags,
+                    kf::PartialArgs& a) {
   int st = check_shape(shape);
   if (st != KF_OK) return st;
   if (num_routes < 0 || num_launch < 0 || max_pages_per_route < 0) return KF_ERR_INVALID_ARG;
@@ -184,7 +185,6 @@ int partial_attn_impl(const kf_shape* shape, const void* q, const void* k_pool, 
       kf::workspace_layout(num_launch, shape->num_kv_heads, group, plan.max_chunks);
   if (!workspace || !aligned(workspace, 256) || workspace_bytes < l.total) return KF_ERR_WORKSPACE;
 
-  kf::PartialArgs a;
   a.q = static_cast<const uint16_t*>(q);
   a.k_pool = k_pool;
   a.v_pool = v_pool;
@@ -211,12 +211,68 @@ int partial_attn_impl(const kf_shape* shape, const void* q, const void* k_pool, 
   a.num_pages = shape->num_pages;
   a.num_page_ids = shape->num_page_ids;
   a.scale_log2 = (float)((double)shape->scale * 1.4426950408889634074);
-  return kf::launch_partial(a, fp8, as_stream(stream)) == hipSuccess ? KF_OK : KF_ERR_HIP;
+  return KF_OK;
+}
+
+int partial_attn_impl(const kf_shape* shape, const void* q, const void* k_pool, const void* v_pool,
+                      const float* k_scale, const float* v_scale, const kf_route* routes,
+                      int32_t num_routes, const int32_t* route_list, int32_t num_launch,
+                      int32_t max_pages_per_route, const int32_t* page_ids, float* o_part,
+                      float* lse_part, void* workspace, size_t workspace_bytes,
+                      int32_t* err_flags, void* stream) {
+  kf::PartialArgs a{};
+  const int st = prepare_partial(shape, q, k_pool, v_pool, k_scale, v_scale, routes, num_routes,
+                                 route_list, num_launch, max_pages_per_route, page_ids, o_part,
+                                 lse_part, workspace, workspace_bytes, err_flags, a);
+  if (st != KF_OK || a.num_units_routes == 0) return st;
+  return kf::launch_partial(a, shape->kv_dtype == KF_KV_FP8_E4M3, as_stream(stream)) == hipSuccess
+             ? KF_OK
+             : KF_ERR_HIP;
+}
+
+// Host checks of kf_merge_partials; fills the kernel arguments.
+int prepare_merge(int32_t num_seqs, int32_t num_routes, int32_t num_q_heads, int32_t head_dim,
+                  const float* o_part, const float* lse_part, const int32_t* seq_route_begin,
+                  float* out, float* lse_out, int32_t* err_flags, kf::MergeArgs& a) {
+  if (num_seqs < 0 || num_routes < 0 || num_q_heads <= 0) return KF_ERR_INVALID_ARG;
+  if (head_dim != KF_HEAD_DIM) return KF_ERR_UNSUPPORTED;
+  if (num_seqs == 0) return KF_OK;
+  if (num_seqs > 65535 || num_q_heads > 65535) return KF_ERR_UNSUPPORTED;
+  if (!seq_route_begin || !out || !lse_out || !err_flags ||
+      (num_routes > 0 && (!o_part || !lse_part)))
+    return KF_ERR_INVALID_ARG;
+  if ((o_part && !aligned(o_part, 8)) || !aligned(out, 8)) return KF_ERR_INVALID_ARG;
+  const void* p4[] = {lse_part, seq_route_begin, lse_out, err_flags};
+  for (const void* p : p4)
+    if (p && !aligned(p, 4)) return KF_ERR_INVALID_ARG;
+  a.o_part = o_part;
+  a.lse_part = lse_part;
+  a.seq_route_begin = seq_route_begin;
+  a.out = out;
+  a.lse_out = lse_out;
+  a.err_flags = err_flags;
+  a.num_seqs = num_seqs;
+  a.num_routes = num_routes;
+  a.num_q_heads = num_q_heads;
+  return KF_OK;
 }
 
 }  // namespace
 
 extern "C" {
+
+int kf_kv_append(const kf_shape* shape, void* k_pool, void* v_pool, float* k_scale,
+                 float* v_scale, const void* k_new, const void* v_new, kf_route* routes,
+                 int32_t num_routes, const int32_t* tail_route, const int32_t* page_ids,
+                 int32_t* err_flags, void* stream) {
+  kf::AppendArgs a{};
+  const int st = prepare_append(shape, k_pool, v_pool, k_scale, v_scale, k_new, v_new, routes,
+                                num_routes, tail_route, page_ids, err_flags, a);
+  if (st != KF_OK || shape->num_seqs == 0) return st;
+  return kf::launch_append(a, shape->kv_dtype == KF_KV_FP8_E4M3, as_stream(stream)) == hipSuccess
+             ? KF_OK
+             : KF_ERR_HIP;
+}
 
 int kf_partial_attn(const kf_shape* shape, const void* q, const void* k_pool, const void* v_pool,
                     const float* k_scale, const float* v_scale, const kf_route* routes,
@@ -243,28 +299,51 @@ int kf_partial_attn_subset(const kf_shape* shape, const void* q, const void* k_p
 int kf_merge_partials(int32_t num_seqs, int32_t num_routes, int32_t num_q_heads, int32_t head_dim,
                       const float* o_part, const float* lse_part, const int32_t* seq_route_begin,
                       float* out, float* lse_out, int32_t* err_flags, void* stream) {
-  if (num_seqs < 0 || num_routes < 0 || num_q_heads <= 0) return KF_ERR_INVALID_ARG;
-  if (head_dim != KF_HEAD_DIM) return KF_ERR_UNSUPPORTED;
-  if (num_seqs == 0) return KF_OK;
-  if (num_seqs > 65535 || num_q_heads > 65535) return KF_ERR_UNSUPPORTED;
-  if (!seq_route_begin || !out || !lse_out || !err_flags ||
-      (num_routes > 0 && (!o_part || !lse_part)))
-    return KF_ERR_INVALID_ARG;
-  if ((o_part && !aligned(o_part, 8)) || !aligned(out, 8)) return KF_ERR_INVALID_ARG;
-  const void* p4[] = {lse_part, seq_route_begin, lse_out, err_flags};
-  for (const void* p : p4)
-    if (p && !aligned(p, 4)) return KF_ERR_INVALID_ARG;
-  kf::MergeArgs a;
-  a.o_part = o_part;
-  a.lse_part = lse_part;
-  a.seq_route_begin = seq_route_begin;
-  a.out = out;
-  a.lse_out = lse_out;
-  a.err_flags = err_flags;
-  a.num_seqs = num_seqs;
-  a.num_routes = num_routes;
-  a.num_q_heads = num_q_heads;
+  kf::MergeArgs a{};
+  const int st = prepare_merge(num_seqs, num_routes, num_q_heads, head_dim, o_part, lse_part,
+                               seq_route_begin, out, lse_out, err_flags, a);
+  if (st != KF_OK || num_seqs == 0) return st;
   return kf::launch_merge(a, as_stream(stream)) == hipSuccess ? KF_OK : KF_ERR_HIP;
+}
+
+int kf_decode_step(const kf_shape* shape, const void* q, void* k_pool, void* v_pool,
+                   float* k_scale, float* v_scale, const void* k_new, const void* v_new,
+                   kf_route* routes, int32_t num_routes, const int32_t* tail_route,
+                   int32_t max_pages_per_route, const int32_t* page_ids,
+                   const int32_t* seq_route_begin, float* o_part, float* lse_part, float* out,
+                   float* lse_out, void* workspace, size_t workspace_bytes, int32_t* err_flags,
+                   void* stream) {
+  kf::AppendArgs ap{};
+  kf::PartialArgs pa{};
+  kf::MergeArgs ma{};
+  int st = prepare_append(shape, k_pool, v_pool, k_scale, v_scale, k_new, v_new, routes,
+                          num_routes, tail_route, page_ids, err_flags, ap);
+  if (st != KF_OK) return st;
+  st = prepare_partial(shape, q, k_pool, v_pool, k_scale, v_scale, routes, num_routes, nullptr,
+                       num_routes, max_pages_per_route, page_ids, o_part, lse_part, workspace,
+                       workspace_bytes, err_flags, pa);
+  if (st != KF_OK) return st;
+  st = prepare_merge(shape->num_seqs, num_routes, shape->num_q_heads, shape->head_dim, o_part,
+                     lse_part, seq_route_begin, out, lse_out, err_flags, ma);
+  if (st != KF_OK || shape->num_seqs == 0) return st;
+  const hipStream_t s = as_stream(stream);
+  const bool fp8 = shape->kv_dtype == KF_KV_FP8_E4M3;
+  if (fp8) {  // fp8 pages may be re-encoded by an append: keep the separate append kernel
+    if (kf::launch_append(ap, true, s) != hipSuccess) return KF_ERR_HIP;
+  } else {
+    pa.k_new = ap.k_new;
+    pa.v_new = ap.v_new;
+    pa.tail_route = tail_route;
+    pa.k_pool_w = static_cast<uint16_t*>(k_pool);
+    pa.v_pool_w = static_cast<uint16_t*>(v_pool);
+    ma.routes = routes;
+    ma.tail_route = tail_route;
+    ma.page_ids = page_ids;
+    ma.num_pages = shape->num_pages;
+    ma.num_page_ids = shape->num_page_ids;
+  }
+  if (pa.num_units_routes > 0 && kf::launch_partial(pa, fp8, s) != hipSuccess) return KF_ERR_HIP;
+  return kf::launch_merge(ma, s) == hipSuccess ? KF_OK : KF_ERR_HIP;
 }
 
 }  // extern "C"

@@ -214,9 +214,26 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
 struct RouteView {
   int seq, n, npages, base;
   bool bad;
+  bool app;       // fused step: this route takes the step's token (local index n - 1)
+  int app_pid;    // page id and slot that receive it
+  int app_slot;
 };
 
-// Route row r as the kernels see it, with the device-side consistency checks.
+// The append rule of append_kernel, seen from the route: route r takes the
+// step's token iff it is its sequence's tail and the token's page is
+// reserved, listed and inside the pool.  The merge kernel takes the same
+// decision from the sequence side (tail_append_status).
+__device__ __forceinline__ bool fused_append(const PartialArgs& a, int r, int seq, int j, int base,
+                                             int cap, int& pid) {
+  if (!a.tail_route || seq < 0 || seq >= a.num_seqs || a.tail_route[seq] != r) return false;
+  if (j < 0 || j / kPage >= cap || base < 0 || (int64_t)base + j / kPage >= a.num_page_ids)
+    return false;
+  pid = a.page_ids[base + j / kPage];
+  return pid >= 0 && pid < a.num_pages;
+}
+
+// Route row r as the kernels see it, with the device-side consistency checks
+// (in a fused step, after the step's append).
 __device__ __forceinline__ RouteView read_route(const PartialArgs& a, int r) {
   const int32_t* rp = reinterpret_cast<const int32_t*>(a.routes + r);
   RouteView v;
@@ -224,10 +241,32 @@ __device__ __forceinline__ RouteView read_route(const PartialArgs& a, int r) {
   const int tb = rp[2], te = rp[3], cap = rp[5];
   v.base = rp[4];
   v.n = te - tb;
+  v.app_pid = 0;
+  v.app = fused_append(a, r, v.seq, v.n, v.base, cap, v.app_pid);
+  v.app_slot = v.n & (kPage - 1);
+  if (v.app) v.n += 1;
   v.npages = v.n > 0 ? (v.n + kPage - 1) / kPage : 0;
   v.bad = v.seq < 0 || v.seq >= a.num_seqs || v.n < 0 || v.base < 0 || v.npages > cap ||
           v.npages > a.max_pages_per_route || (int64_t)v.base + v.npages > a.num_page_ids;
   return v;
+}
+
+// Fused step: write the step's token of KV head g into the route's page,
+// then make it visible to every wave of this workgroup before any of them
+// loads the page (waves of a workgroup share the compute unit's L1).
+__device__ __forceinline__ void write_new_token(const PartialArgs& a, const RouteView& rv, int g,
+                                                int tid) {
+  const int H = a.num_kv_heads;
+  const uint16_t* kn = a.k_new + ((size_t)rv.seq * H + g) * kDim;
+  const uint16_t* vn = a.v_new + ((size_t)rv.seq * H + g) * kDim;
+  const size_t head = (size_t)rv.app_pid * H + g;
+  if (tid < kDim) {
+    a.k_pool_w[(head * kPage + rv.app_slot) * kDim + tid] = kn[tid];
+    a.v_pool_w[(head * kDim + tid) * kPage + rv.app_slot] = vn[tid];
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __syncthreads();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
 // Tile geometry.  A wave tile is TP pages: 2 for bf16 (16 KiB of K+V), 4 for
@@ -300,6 +339,8 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
   const RouteView rv = read_route(a, r);
   if (rv.bad || rv.npages == 0) {
     if (c == 0) {
+      if constexpr (!FP8)
+        if (rv.app) write_new_token(a, rv, g, tid);  // the pool takes the token all the same
       const float ov = rv.bad ? qnan() : 0.0f, lv = rv.bad ? qnan() : neg_inf();
       for (int e = tid; e < G * kDim; e += kThreads)
         a.o_part[((size_t)r * Hq + hq0 + e / kDim) * kDim + e % kDim] = ov;
@@ -311,6 +352,8 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
   const int seq = rv.seq, n = rv.n, npages = rv.npages;
   const int nchunks = (npages + a.chunk_pages - 1) / a.chunk_pages;
   if (c >= nchunks) return;
+  if constexpr (!FP8)
+    if (rv.app && c == nchunks - 1) write_new_token(a, rv, g, tid);  // the chunk with the last page
   const int p0 = (int)((int64_t)c * npages / nchunks);
   const int p1 = (int)((int64_t)(c + 1) * npages / nchunks);
   const int ntiles = (p1 - p0 + TP - 1) / TP;
@@ -632,10 +675,36 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(PartialArgs a) {
 }
 
 // -------------------------------------------------------------------- merge
+// The append decision of sequence b in a fused step, with append_kernel's
+// checks and flags: 0 = no append, 1 = appended, else an error flag.
+__device__ __forceinline__ int tail_append_status(const MergeArgs& a, int b, int& r) {
+  r = a.tail_route[b];
+  if (r < 0) return 0;
+  if (r >= a.num_routes) return KF_EFLAG_BAD_ROUTE << 8;
+  const int32_t* rp = reinterpret_cast<const int32_t*>(a.routes + r);
+  const int seq = rp[0], tb = rp[2], te = rp[3], base = rp[4], cap = rp[5];
+  const int j = te - tb;
+  if (seq != b || j < 0) return KF_EFLAG_BAD_ROUTE << 8;
+  if (j / kPage >= cap) return KF_EFLAG_TAIL_FULL << 8;
+  if (base < 0 || (int64_t)base + j / kPage >= a.num_page_ids) return KF_EFLAG_BAD_ROUTE << 8;
+  const int pid = a.page_ids[base + j / kPage];
+  if (pid < 0 || pid >= a.num_pages) return KF_EFLAG_BAD_PAGE << 8;
+  return 1;
+}
+
 // One wave per (query head, sequence); lane holds dims 2*lane, 2*lane+1.
+// In a fused step, wave (0, b) also advances sequence b's tail.
 __global__ __launch_bounds__(64) void merge_kernel(MergeArgs a) {
   const int h = blockIdx.x, b = blockIdx.y, lane = threadIdx.x;
   const int Hq = a.num_q_heads;
+  if (a.tail_route && h == 0 && lane == 0) {
+    int r = 0;
+    const int st = tail_append_status(a, b, r);
+    if (st == 1)
+      a.routes[r].tok_end += 1;  // no other wave of this launch reads it
+    else if (st)
+      atomicOr(a.err_flags, st >> 8);
+  }
   const int r0 = a.seq_route_begin[b], r1 = a.seq_route_begin[b + 1];
   float2* out = reinterpret_cast<float2*>(a.out + ((size_t)b * Hq + h) * kDim) + lane;
   float* lse_out = a.lse_out + (size_t)b * Hq + h;

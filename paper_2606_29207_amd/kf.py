@@ -33,7 +33,8 @@ EFLAG_BAD_PAGE = 4
 
 # every symbol include/kf.h declares
 EXPORTS = ("kf_kv_append", "kf_partial_attn_workspace_bytes", "kf_partial_attn",
-           "kf_partial_attn_subset", "kf_merge_partials", "kf_status_str", "kf_version")
+           "kf_partial_attn_subset", "kf_merge_partials", "kf_decode_step", "kf_status_str",
+           "kf_version")
 
 
 class KFError(RuntimeError):
@@ -78,6 +79,9 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.kf_partial_attn_subset.restype = ctypes.c_int
     lib.kf_merge_partials.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]
     lib.kf_merge_partials.restype = ctypes.c_int
+    lib.kf_decode_step.argtypes = [sp, vp, vp, vp, vp, vp, vp, vp, vp, i32, vp, i32, vp, vp, vp, vp,
+                                   vp, vp, vp, sz, vp, vp]
+    lib.kf_decode_step.restype = ctypes.c_int
     lib.kf_status_str.argtypes = [ctypes.c_int]
     lib.kf_status_str.restype = ctypes.c_char_p
     lib.kf_version.argtypes = []
@@ -250,3 +254,44 @@ def merge_partials(num_seqs, o_part, lse_part, seq_route_begin, out, lse_out, er
                                _ptr(seq_route_begin), _ptr(out), _ptr(lse_out),
                                _ptr(err_flags), _stream(stream))
     _check(st, "kf_merge_partials")
+
+
+def decode_step(shape: Shape, q, k_pool, v_pool, k_new, v_new, routes, tail_route,
+                max_pages_per_route, page_ids, seq_route_begin, o_part, lse_part, out, lse_out,
+                workspace, err_flags, k_scale=None, v_scale=None, stream=None):
+    """kf_decode_step: append -> partial attention -> merge in one call (two
+    launches for bf16 pools).  Arguments as for kv_append, partial_attn and
+    merge_partials."""
+    lib = load()
+    for t, n in ((q, "q"), (k_pool, "k_pool"), (v_pool, "v_pool"), (k_new, "k_new"),
+                 (v_new, "v_new"), (routes, "routes"), (tail_route, "tail_route"),
+                 (page_ids, "page_ids"), (seq_route_begin, "seq_route_begin"), (o_part, "o_part"),
+                 (lse_part, "lse_part"), (out, "out"), (lse_out, "lse_out"),
+                 (workspace, "workspace"), (err_flags, "err_flags")):
+        _dev(t, n)
+    B, Hq, H, R = shape.num_seqs, shape.num_q_heads, shape.num_kv_heads, routes.shape[0]
+    _need(tuple(q.shape) == (B, Hq, HEAD_DIM) and q.element_size() == 2,
+          "q must be bf16 [num_seqs, num_q_heads, 128]")
+    _need(tuple(k_new.shape) == (B, H, HEAD_DIM) and tuple(v_new.shape) == (B, H, HEAD_DIM)
+          and k_new.element_size() == 2 and v_new.element_size() == 2,
+          "k_new/v_new must be bf16 [num_seqs, num_kv_heads, 128]")
+    _need(tail_route.numel() >= B and tail_route.dtype == torch.int32, "tail_route: int32 [num_seqs]")
+    _need(seq_route_begin.dtype == torch.int32 and seq_route_begin.numel() >= B + 1,
+          "seq_route_begin must be int32 [num_seqs + 1]")
+    for t, shp, n in ((o_part, (R, Hq, HEAD_DIM), "o_part"), (lse_part, (R, Hq), "lse_part"),
+                      (out, (B, Hq, HEAD_DIM), "out"), (lse_out, (B, Hq), "lse_out")):
+        _need(tuple(t.shape) == shp and t.dtype == torch.float32, f"{n} must be float32 {list(shp)}")
+    _check_tables(shape, k_pool, v_pool, routes, page_ids)
+    if shape.kv_dtype == KV_FP8_E4M3:
+        for t, n in ((k_scale, "k_scale"), (v_scale, "v_scale")):
+            _need(t is not None, f"{n} is required for fp8 pools")
+            _dev(t, n)
+            _need(t.dtype == torch.float32 and t.numel() >= shape.num_pages * shape.num_kv_heads,
+                  f"{n} must be float32 [num_pages, num_kv_heads]")
+    st = lib.kf_decode_step(ctypes.byref(shape), _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(k_scale),
+                            _ptr(v_scale), _ptr(k_new), _ptr(v_new), _ptr(routes), R,
+                            _ptr(tail_route), int(max_pages_per_route), _ptr(page_ids),
+                            _ptr(seq_route_begin), _ptr(o_part), _ptr(lse_part), _ptr(out),
+                            _ptr(lse_out), _ptr(workspace), workspace.numel(), _ptr(err_flags),
+                            _stream(stream))
+    _check(st, "kf_decode_step")

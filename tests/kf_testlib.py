@@ -39,8 +39,9 @@ def run_oracle(inst, steps=1, tail_route=None, new_tokens=None):
                 lse_part=lse_part, out=out, lse=lse, flags=flags | f1 | f2)
 
 
-def run_gpu(inst, steps=1, tail_route=None, nan_fill=True, new_tokens=None):
-    """HIP path: the same sequence of calls through the C ABI."""
+def run_gpu(inst, steps=1, tail_route=None, nan_fill=True, new_tokens=None, fused=False):
+    """HIP path: the same sequence of calls through the C ABI (fused: one
+    kf_decode_step per step)."""
     import torch
     new_tokens = new_tokens or inst.new_tokens
     from paper_2606_29207_amd.step import DecodeState
@@ -53,7 +54,10 @@ def run_gpu(inst, steps=1, tail_route=None, nan_fill=True, new_tokens=None):
                 t.fill_(float("nan"))
         if inst.wl.appends:
             kn, vn = st.upload_new_tokens(*new_tokens(s))
-            st.step(kn, vn)
+            if fused:
+                st.step_fused(kn, vn)
+            else:
+                st.step(kn, vn)
         else:
             st.step()
     torch.cuda.synchronize()

@@ -130,6 +130,40 @@ def test_append_host_checks(lib):
     assert lib.kf_kv_append(ctypes.byref(s0), *([None] * 6), None, 0, None, None, None, None) == 0
 
 
+def _step(lib, shape, **kw):
+    p = dict(q=FAKE, k=FAKE, v=FAKE, ks=None, vs=None, kn=FAKE, vn=FAKE, routes=FAKE, R=4,
+             tail=FAKE, maxp=8, pids=FAKE, srb=FAKE, o=FAKE, lse=FAKE, out=FAKE, lse_out=FAKE,
+             ws=FAKE, wsb=1 << 30, flags=FAKE)
+    p.update(kw)
+    v = lambda x: None if x is None else ctypes.c_void_p(x)  # noqa: E731
+    return lib.kf_decode_step(ctypes.byref(shape), v(p["q"]), v(p["k"]), v(p["v"]), v(p["ks"]),
+                              v(p["vs"]), v(p["kn"]), v(p["vn"]), v(p["routes"]), p["R"],
+                              v(p["tail"]), p["maxp"], v(p["pids"]), v(p["srb"]), v(p["o"]),
+                              v(p["lse"]), v(p["out"]), v(p["lse_out"]), v(p["ws"]), p["wsb"],
+                              v(p["flags"]), None)
+
+
+@pytest.mark.parametrize("shape_kw,call_kw,status", [
+    ({}, dict(kn=None), -1),                  # append arguments
+    ({}, dict(tail=FAKE + 2), -1),
+    ({"kv_dtype": 1}, {}, -1),                # fp8 without scales
+    ({}, dict(q=None), -1),                   # partial arguments
+    ({}, dict(wsb=16), -3),
+    ({}, dict(R=70000), -2),
+    ({}, dict(srb=None), -1),                 # merge arguments
+    ({}, dict(out=FAKE + 4), -1),
+    ({"head_dim": 64}, {}, -2),
+])
+def test_decode_step_host_checks(lib, shape_kw, call_kw, status):
+    """Every check of the three calls runs before anything is launched (with
+    these fake pointers a launch would fault)."""
+    assert _step(lib, _shape(**shape_kw), **call_kw) == status
+
+
+def test_decode_step_no_sequences_is_a_no_op(lib):
+    assert _step(lib, _shape(num_seqs=0), R=0) == 0
+
+
 def test_merge_host_checks(lib):
     v = ctypes.c_void_p
     ok = [v(FAKE)] * 7
