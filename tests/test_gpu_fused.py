@@ -131,3 +131,33 @@ def test_fused_fullsize_llama_sampled(gpu):
     inst = make_instance(workload("llama8b_32k"), seed=1, steps=2)
     same_bits(host(run_gpu(inst, 2, fused=True, nan_fill=False)),
               host(run_gpu(inst, 2, nan_fill=False)))
+
+
+def test_fused_tail_crossing_max_pages(gpu):
+    """A tail full to its last page takes a token on a new page beyond
+    max_pages_per_route: the token is stored, the route's partial is NaN with
+    KF_EFLAG_BAD_ROUTE, exactly as with the three calls."""
+    import torch
+    from paper_2606_29207_amd.step import DecodeState
+    wl = workload("llama8b_32k", num_seqs=2, num_q_heads=8, num_kv_heads=2, part_tokens=256,
+                  appends=1)
+    inst = make_instance(wl, seed=8, steps=1, seq_lens=[512, 320])   # seq 0's tail: 16 full pages
+    assert inst.max_pages_per_route == 17
+    outs = []
+    for fused in (False, True):
+        st = DecodeState(q=inst.q, k_pool=inst.k_pool, v_pool=inst.v_pool, routes=inst.routes,
+                         page_ids=inst.page_ids, seq_route_begin=inst.seq_route_begin,
+                         tail_route=inst.tail_route, scale=inst.scale, max_pages_per_route=16)
+        kn, vn = st.upload_new_tokens(*inst.new_tokens(0))
+        (st.step_fused if fused else st.step)(kn, vn)
+        torch.cuda.synchronize()
+        outs.append(host(st))
+    same_bits(outs[1], outs[0])
+    kp, vp, rt, f0 = oracle.kv_append(inst.k_pool, inst.v_pool, inst.routes.copy(), inst.page_ids,
+                                      inst.tail_route, *inst.new_tokens(0))
+    o_part, lse_part, f1 = oracle.partial_attn(inst.q, kp, vp, rt, inst.page_ids, num_kv_heads=2,
+                                               scale=inst.scale, max_pages_per_route=16)
+    out, lse, f2 = oracle.merge_partials(o_part, lse_part, inst.seq_route_begin)
+    assert f0 == 0 and f1 | f2 == oracle.EFLAG_BAD_ROUTE
+    compare_all(outs[1], dict(k_pool=kp, v_pool=vp, k_scale=None, v_scale=None, routes=rt,
+                              o_part=o_part, lse_part=lse_part, out=out, lse=lse, flags=f1 | f2))
