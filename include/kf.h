@@ -218,6 +218,26 @@ int kf_decode_step(const kf_shape* shape, const void* q, void* k_pool, void* v_p
                    float* lse_out, void* workspace, size_t workspace_bytes, int32_t* err_flags,
                    void* stream);
 
+/*
+ * kf_debug_gather -- test export: the resident tokens of route `route`
+ * gathered through the routing table by the same route checks and page
+ * lookup the attention kernels use (Section 4.1, one route = one token range
+ * and the pages that hold it).  With n = min(tok_end - tok_begin,
+ * max_tokens), token j < n of the route sits in page
+ * page_ids[page_base + j / 16], slot j % 16, and out_k[j][g][:],
+ * out_v[j][g][:] receive its K and V elements for every KV head g (bf16 bits,
+ * or E4M3 codes for fp8 pools; scales are not applied).  Rows j >= n are not
+ * written.  A route row failing kf_partial_attn's checks sets
+ * KF_EFLAG_BAD_ROUTE and writes nothing; a page id outside the pool sets
+ * KF_EFLAG_BAD_PAGE and leaves that page's rows unwritten.  route must lie in
+ * [0, num_routes) (else KF_ERR_INVALID_ARG).  out_k/out_v: device
+ * [max_tokens][num_kv_heads][128] elements.  Alignment: 4 bytes.
+ */
+int kf_debug_gather(const kf_shape* shape, const void* k_pool, const void* v_pool,
+                    const kf_route* routes, int32_t num_routes, int32_t route,
+                    int32_t max_pages_per_route, const int32_t* page_ids, int32_t max_tokens,
+                    void* out_k, void* out_v, int32_t* err_flags, void* stream);
+
 /* Static description of a status code (never NULL). */
 const char* kf_status_str(int status);
 

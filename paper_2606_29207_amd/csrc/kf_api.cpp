@@ -306,6 +306,41 @@ int kf_merge_partials(int32_t num_seqs, int32_t num_routes, int32_t num_q_heads,
   return kf::launch_merge(a, as_stream(stream)) == hipSuccess ? KF_OK : KF_ERR_HIP;
 }
 
+int kf_debug_gather(const kf_shape* shape, const void* k_pool, const void* v_pool,
+                    const kf_route* routes, int32_t num_routes, int32_t route,
+                    int32_t max_pages_per_route, const int32_t* page_ids, int32_t max_tokens,
+                    void* out_k, void* out_v, int32_t* err_flags, void* stream) {
+  const int st = check_shape(shape);
+  if (st != KF_OK) return st;
+  if (num_routes < 0 || route < 0 || route >= num_routes || max_pages_per_route < 0 ||
+      max_tokens < 0)
+    return KF_ERR_INVALID_ARG;
+  if (!k_pool || !v_pool || !routes || !err_flags || (shape->num_page_ids > 0 && !page_ids) ||
+      (max_tokens > 0 && (!out_k || !out_v)))
+    return KF_ERR_INVALID_ARG;
+  const void* p4[] = {k_pool, v_pool, routes, page_ids, out_k, out_v, err_flags};
+  for (const void* p : p4)
+    if (p && !aligned(p, 4)) return KF_ERR_INVALID_ARG;
+  if (max_tokens == 0) return KF_OK;
+  kf::PartialArgs a{};
+  a.k_pool = k_pool;
+  a.v_pool = v_pool;
+  a.routes = routes;
+  a.page_ids = page_ids;
+  a.err_flags = err_flags;
+  a.num_seqs = shape->num_seqs;
+  a.num_q_heads = shape->num_q_heads;
+  a.num_kv_heads = shape->num_kv_heads;
+  a.num_routes = num_routes;
+  a.max_pages_per_route = max_pages_per_route;
+  a.num_pages = shape->num_pages;
+  a.num_page_ids = shape->num_page_ids;
+  return kf::launch_gather(a, shape->kv_dtype == KF_KV_FP8_E4M3, route, max_tokens, out_k, out_v,
+                           as_stream(stream)) == hipSuccess
+             ? KF_OK
+             : KF_ERR_HIP;
+}
+
 int kf_decode_step(const kf_shape* shape, const void* q, void* k_pool, void* v_pool,
                    float* k_scale, float* v_scale, const void* k_new, const void* v_new,
                    kf_route* routes, int32_t num_routes, const int32_t* tail_route,

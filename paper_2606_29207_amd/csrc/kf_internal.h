@@ -97,5 +97,7 @@ WorkspaceLayout workspace_layout(int32_t num_routes, int32_t num_kv_heads, int32
 hipError_t launch_append(const AppendArgs& a, bool fp8, hipStream_t stream);
 hipError_t launch_partial(const PartialArgs& a, bool fp8, hipStream_t stream);
 hipError_t launch_merge(const MergeArgs& a, hipStream_t stream);
+hipError_t launch_gather(const PartialArgs& a, bool fp8, int route, int max_tokens, void* out_k,
+                         void* out_v, hipStream_t stream);
 
 }  // namespace kf

@@ -674,6 +674,38 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(PartialArgs a) {
   if (tid < G) a.lse_part[(size_t)r * Hq + hq0 + tid] = (s_fm[tid] + __log2f(s_fl[tid])) * kLn2;
 }
 
+// ------------------------------------------------------------------- gather
+// Test export: the resident tokens of one route copied out through the same
+// route checks (read_route) and page lookup as the attention kernels.  Block
+// p copies route-local page p: out[j][g][:] for j = 16 p + slot.
+template <class T>
+__global__ __launch_bounds__(256) void gather_kernel(PartialArgs a, int route, int max_tokens,
+                                                     T* out_k, T* out_v) {
+  const int p = blockIdx.x, tid = threadIdx.x, H = a.num_kv_heads;
+  const RouteView rv = read_route(a, route);
+  if (rv.bad) {
+    if (p == 0 && tid == 0) atomicOr(a.err_flags, KF_EFLAG_BAD_ROUTE);
+    return;
+  }
+  const int n = min(rv.n, max_tokens);
+  if (p * kPage >= n) return;
+  const int pid = a.page_ids[rv.base + p];
+  if (pid < 0 || pid >= a.num_pages) {
+    if (tid == 0) atomicOr(a.err_flags, KF_EFLAG_BAD_PAGE);
+    return;
+  }
+  const T* kp = static_cast<const T*>(a.k_pool);
+  const T* vp = static_cast<const T*>(a.v_pool);
+  for (int e = tid; e < H * kPage * kDim; e += blockDim.x) {
+    const int g = e / (kPage * kDim), slot = (e / kDim) % kPage, d = e % kDim;
+    const int j = p * kPage + slot;
+    if (j >= n) continue;
+    const size_t head = (size_t)pid * H + g;
+    out_k[((size_t)j * H + g) * kDim + d] = kp[(head * kPage + slot) * kDim + d];
+    out_v[((size_t)j * H + g) * kDim + d] = vp[(head * kDim + d) * kPage + slot];
+  }
+}
+
 // -------------------------------------------------------------------- merge
 // The append decision of sequence b in a fused step, with append_kernel's
 // checks and flags: 0 = no append, 1 = appended, else an error flag.
@@ -764,6 +796,19 @@ hipError_t launch_partial(const PartialArgs& a, bool fp8, hipStream_t stream) {
   if (e != hipSuccess || a.max_chunks == 1) return e;
   hipLaunchKernelGGL(combine_kernel, dim3(a.num_kv_heads, a.num_units_routes), dim3(kThreads), 0,
                      stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(const PartialArgs& a, bool fp8, int route, int max_tokens, void* out_k,
+                         void* out_v, hipStream_t stream) {
+  const int blocks = (max_tokens + kPage - 1) / kPage;
+  if (blocks == 0) return hipSuccess;
+  if (fp8)
+    hipLaunchKernelGGL(gather_kernel<uint8_t>, dim3(blocks), dim3(256), 0, stream, a, route,
+                       max_tokens, static_cast<uint8_t*>(out_k), static_cast<uint8_t*>(out_v));
+  else
+    hipLaunchKernelGGL(gather_kernel<uint16_t>, dim3(blocks), dim3(256), 0, stream, a, route,
+                       max_tokens, static_cast<uint16_t*>(out_k), static_cast<uint16_t*>(out_v));
   return hipGetLastError();
 }
 

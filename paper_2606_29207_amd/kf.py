@@ -33,8 +33,8 @@ EFLAG_BAD_PAGE = 4
 
 # every symbol include/kf.h declares
 EXPORTS = ("kf_kv_append", "kf_partial_attn_workspace_bytes", "kf_partial_attn",
-           "kf_partial_attn_subset", "kf_merge_partials", "kf_decode_step", "kf_status_str",
-           "kf_version")
+           "kf_partial_attn_subset", "kf_merge_partials", "kf_decode_step", "kf_debug_gather",
+           "kf_status_str", "kf_version")
 
 
 class KFError(RuntimeError):
@@ -82,6 +82,8 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.kf_decode_step.argtypes = [sp, vp, vp, vp, vp, vp, vp, vp, vp, i32, vp, i32, vp, vp, vp, vp,
                                    vp, vp, vp, sz, vp, vp]
     lib.kf_decode_step.restype = ctypes.c_int
+    lib.kf_debug_gather.argtypes = [sp, vp, vp, vp, i32, i32, i32, vp, i32, vp, vp, vp, vp]
+    lib.kf_debug_gather.restype = ctypes.c_int
     lib.kf_status_str.argtypes = [ctypes.c_int]
     lib.kf_status_str.restype = ctypes.c_char_p
     lib.kf_version.argtypes = []
@@ -295,3 +297,23 @@ def decode_step(shape: Shape, q, k_pool, v_pool, k_new, v_new, routes, tail_rout
                             _ptr(lse_out), _ptr(workspace), workspace.numel(), _ptr(err_flags),
                             _stream(stream))
     _check(st, "kf_decode_step")
+
+
+def debug_gather(shape: Shape, k_pool, v_pool, routes, route, max_pages_per_route, page_ids,
+                 max_tokens, out_k, out_v, err_flags, stream=None):
+    """kf_debug_gather (test export): route ``route``'s tokens through the page
+    table into out_k/out_v [max_tokens, num_kv_heads, 128] (pool element type)."""
+    lib = load()
+    for t, n in ((k_pool, "k_pool"), (v_pool, "v_pool"), (routes, "routes"), (page_ids, "page_ids"),
+                 (out_k, "out_k"), (out_v, "out_v"), (err_flags, "err_flags")):
+        _dev(t, n)
+    _check_tables(shape, k_pool, v_pool, routes, page_ids)
+    shp = (int(max_tokens), shape.num_kv_heads, HEAD_DIM)
+    for t, n in ((out_k, "out_k"), (out_v, "out_v")):
+        _need(tuple(t.shape) == shp and t.element_size() == k_pool.element_size(),
+              f"{n} must be [max_tokens, num_kv_heads, 128] of the pool element type")
+    st = lib.kf_debug_gather(ctypes.byref(shape), _ptr(k_pool), _ptr(v_pool), _ptr(routes),
+                             routes.shape[0], int(route), int(max_pages_per_route), _ptr(page_ids),
+                             int(max_tokens), _ptr(out_k), _ptr(out_v), _ptr(err_flags),
+                             _stream(stream))
+    _check(st, "kf_debug_gather")

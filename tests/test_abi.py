@@ -191,3 +191,18 @@ def test_workspace_bytes(lib):
     assert kf.partial_attn_workspace_bytes(s, 142, 1025) == rup(recs * 2 * 4) + rup(recs * 128 * 4)
     assert kf.partial_attn_workspace_bytes(s, -1, 5) == 0
     assert kf.partial_attn_workspace_bytes(_shape(head_dim=64), 4, 5) == 0
+
+
+def test_debug_gather_host_checks(lib):
+    v = lambda x: None if x is None else ctypes.c_void_p(x)  # noqa: E731
+    s = _shape()
+
+    def call(route=0, R=4, maxp=8, max_tokens=16, out=FAKE):
+        return lib.kf_debug_gather(ctypes.byref(s), v(FAKE), v(FAKE), v(FAKE), R, route, maxp,
+                                   v(FAKE), max_tokens, v(out), v(out), v(FAKE), None)
+    assert call(route=4) == -1           # route outside [0, num_routes)
+    assert call(route=-1) == -1
+    assert call(max_tokens=-3) == -1
+    assert call(out=None) == -1          # outputs needed when max_tokens > 0
+    assert call(out=FAKE + 2) == -1      # misaligned
+    assert call(max_tokens=0, out=None) == 0   # nothing to gather: no launch
