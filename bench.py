@@ -111,7 +111,14 @@ def cpu_baseline(inst, min_s=10.0, max_s=30.0) -> dict:
             if el >= min_s or el >= max_s:
                 break
     el = time.perf_counter() - t0
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), None)
+    except OSError:
+        pass
     return {"value": round(done_bytes / el / 1e9, 4), "unit": "GB/s", "cores": cores,
+            "cpu_model": model,
             "kind": "oracle",
             "sample": f"{done_seqs} sequence(s) of the same instance (all routes x KV heads, "
                       f"fp64 partials + merge, append not timed), {el:.1f} s on {cores} threads, "
@@ -223,7 +230,7 @@ def main(argv=None):
     wl = workload(args.workload)
     K, W = args.steps, args.warmup
     t = time.perf_counter()
-    inst = make_instance(wl, seed=args.seed, steps=W + 2 * K)
+    inst = make_instance(wl, seed=args.seed, steps=W + 3 * K)
     print(f"[bench] generated {wl.name} in {time.perf_counter() - t:.1f}s", file=sys.stderr, flush=True)
 
     cpu = None
@@ -237,7 +244,7 @@ def main(argv=None):
     torch.cuda.set_device(0)
     st = DecodeState.from_instance(inst)
     news = [st.upload_new_tokens(*inst.new_tokens(s)) if wl.appends else (None, None)
-            for s in range(W + 2 * K)]
+            for s in range(W + 3 * K)]
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
     print(f"[bench] uploaded; warmup {W} steps", file=sys.stderr, flush=True)
@@ -293,6 +300,30 @@ def main(argv=None):
         st.merge()
         e[3].record(stream)
     torch.cuda.synchronize()
+
+    # flushed pass: the next K steps as three calls, each after a 512 MiB
+    # scrub write that evicts the 256 MB Infinity Cache (outside the events)
+    flushed = None
+    if not qf:
+        scrub = torch.empty(512 << 20, dtype=torch.uint8, device=st.device)
+        evf = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+        for i in range(K):
+            scrub.fill_(i & 0xFF)
+            e = evf[i]
+            e[0].record(stream)
+            if wl.appends:
+                st.append(*news[W + 2 * K + i])
+            e[1].record(stream)
+            st.partial()
+            e[2].record(stream)
+            st.merge()
+            e[3].record(stream)
+        torch.cuda.synchronize()
+        del scrub
+        med = lambda a, b: round(float(np.median([e[a].elapsed_time(e[b]) for e in evf])) * 1e3, 2)  # noqa: E731
+        flushed = {"scrub_MiB": 512, "append_us_median": med(0, 1) if wl.appends else None,
+                   "partial_attn_us_median": med(1, 2), "merge_us_median": med(2, 3),
+                   "step_us_median": med(0, 3)}
     flags = st.flags()
     if flags:
         print(f"[bench] device error flags {flags}", file=sys.stderr, flush=True)
@@ -347,9 +378,11 @@ def main(argv=None):
         "breakdown_pass": "a second run of K steps as three calls with HIP events around each",
         "breakdown_us": {"append": round(float(t_app.mean()), 2) if wl.appends else None,
                          "partial_attn": round(float(t_par.mean()), 2),
+                         "partial_attn_median": round(float(np.median(t_par)), 2),
                          "partial_attn_p10_p90": [round(float(np.percentile(t_par, 10)), 2),
                                                   round(float(np.percentile(t_par, 90)), 2)],
                          "merge": round(float(t_mrg.mean()), 2)},
+        "flushed": flushed,
         "attn_merge_us": round(float((t_par + t_mrg).mean()), 2),
         "attn_merge_GBps": round(am_b / ((t_par + t_mrg).mean() * 1e-6) / 1e9, 2),
         "bytes_per_step": int(step_b),
