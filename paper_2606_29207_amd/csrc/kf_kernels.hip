@@ -540,9 +540,9 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
   // wave's next tile are in flight.  Between issuing a tile and computing
   // the previous one there is no branch, so the compiler waits only for the
   // tile it computes; tile ids and their page ids are fetched a tile ahead.
-  // Grabs are monotonic, so a tile computed inside the loop always precedes
-  // a tile already handed out and is full; only the exits can hold the
-  // range's last tile and compute masked.
+  // A wave's tile ids increase, so a tile computed inside the loop always
+  // precedes one already issued and is full; only the tile computed after
+  // the loop can be the range's last and is computed masked.
   TileRaw<FP8> ra, rb;
   const std::integral_constant<bool, false> full{};
   const std::integral_constant<bool, true> masked{};
