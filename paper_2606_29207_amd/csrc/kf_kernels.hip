@@ -325,7 +325,21 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
   __shared__ float s_fm[KF_MAX_GROUP];
   __shared__ float s_fl[KF_MAX_GROUP];
 
-  const int c = blockIdx.x, g = blockIdx.y, u = blockIdx.z;  // u: position in the launch
+  const int c = blockIdx.x;
+  int g = blockIdx.y, u = blockIdx.z;  // u: position in the launch
+  if constexpr (FP8) {
+    // Unsplit fp8 units: workgroups are dealt round-robin over the 8 XCDs.
+    // Give XCD k the k-th eighth of the (head, route) space instead, so the
+    // heads of a route, whose per-page scales share cache lines, meet in one
+    // L2 (the fp8 layer reads ~1% faster; bf16 pools gain nothing from it).
+    const unsigned NT = gridDim.y * gridDim.z;
+    if (gridDim.x == 1 && (NT & 7u) == 0) {
+      const unsigned L = blockIdx.y + gridDim.y * blockIdx.z;
+      const unsigned Lp = (L & 7u) * (NT >> 3) + (L >> 3);
+      g = Lp % gridDim.y;
+      u = Lp / gridDim.y;
+    }
+  }
   const int G = a.group, Hq = a.num_q_heads, H = a.num_kv_heads;
   const int tid = threadIdx.x, lane = tid & 63, grp = lane >> 4, li = lane & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
