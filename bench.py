@@ -212,7 +212,7 @@ def main(argv=None):
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB")
     ap.add_argument("--schedule", choices=("fused", "serial", "query_first"), default="fused",
                     help="fused: kf_decode_step (append fused into the partial-attention "
-                         "launch for bf16 pools, then the merge); serial: append -> partial -> "
+                         "launch, then the merge); serial: append -> partial -> "
                          "merge as three calls on one stream; query_first: historical partials "
                          "from q alone on one stream, append + tail partials on a second, merge "
                          "after both")

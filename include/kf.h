@@ -203,12 +203,12 @@ int kf_merge_partials(int32_t num_seqs, int32_t num_routes, int32_t num_q_heads,
  * merge, with the results, flags and route updates of
  *   kf_kv_append -> kf_partial_attn -> kf_merge_partials
  * on the same arguments (each argument as documented there; the workspace
- * is sized by kf_partial_attn_workspace_bytes).  bf16 pools run it in two
- * launches instead of three: the workgroup that attends over a tail's last
- * page first writes the step's token into it and attends over it, and the
- * merge advances the tails' tok_end and raises the append's flags.  fp8
- * pools run the three kernels (an append may re-encode a whole page).
- * All host checks of the three calls are made before anything is launched.
+ * is sized by kf_partial_attn_workspace_bytes), in two launches instead of
+ * three: the workgroup that attends over a tail's last page first writes the
+ * step's token into it (for fp8 pools by the E4M3 append rule, re-encoding
+ * the page if needed) and attends over it, and the merge advances the tails'
+ * tok_end and raises the append's flags.  All host checks of the three calls
+ * are made before anything is launched.
  */
 int kf_decode_step(const kf_shape* shape, const void* q, void* k_pool, void* v_pool,
                    float* k_scale, float* v_scale, const void* k_new, const void* v_new,

@@ -363,21 +363,23 @@ int kf_decode_step(const kf_shape* shape, const void* q, void* k_pool, void* v_p
   if (st != KF_OK || shape->num_seqs == 0) return st;
   const hipStream_t s = as_stream(stream);
   const bool fp8 = shape->kv_dtype == KF_KV_FP8_E4M3;
-  if (fp8) {  // fp8 pages may be re-encoded by an append: keep the separate append kernel
-    if (kf::launch_append(ap, true, s) != hipSuccess) return KF_ERR_HIP;
-  } else {
-    pa.k_new = ap.k_new;
-    pa.v_new = ap.v_new;
-    pa.tail_route = tail_route;
-    pa.k_pool_w = static_cast<uint16_t*>(k_pool);
-    pa.v_pool_w = static_cast<uint16_t*>(v_pool);
-    ma.routes = routes;
-    ma.tail_route = tail_route;
-    ma.page_ids = page_ids;
-    ma.num_pages = shape->num_pages;
-    ma.num_page_ids = shape->num_page_ids;
+  if (num_routes == 0) {  // nothing to attend: the append kernel raises the flags
+    if (kf::launch_append(ap, fp8, s) != hipSuccess) return KF_ERR_HIP;
+    return kf::launch_merge(ma, s) == hipSuccess ? KF_OK : KF_ERR_HIP;
   }
-  if (pa.num_units_routes > 0 && kf::launch_partial(pa, fp8, s) != hipSuccess) return KF_ERR_HIP;
+  pa.k_new = ap.k_new;
+  pa.v_new = ap.v_new;
+  pa.tail_route = tail_route;
+  pa.k_pool_w = k_pool;
+  pa.v_pool_w = v_pool;
+  pa.k_scale_w = k_scale;
+  pa.v_scale_w = v_scale;
+  ma.routes = routes;
+  ma.tail_route = tail_route;
+  ma.page_ids = page_ids;
+  ma.num_pages = shape->num_pages;
+  ma.num_page_ids = shape->num_page_ids;
+  if (kf::launch_partial(pa, fp8, s) != hipSuccess) return KF_ERR_HIP;
   return kf::launch_merge(ma, s) == hipSuccess ? KF_OK : KF_ERR_HIP;
 }
 

@@ -51,14 +51,16 @@ struct PartialArgs {
   int32_t chunk_pages, max_chunks;  // a unit of n pages uses ceil(n / chunk_pages) workgroups
   int32_t num_pages, num_page_ids;
   float scale_log2;     // scale * log2(e): scores are kept in the base-2 domain
-  // Fused tail append (kf_decode_step, bf16 pools; all NULL otherwise): the
-  // route that is its sequence's tail takes the step's token into its pages
-  // and attends over it; routes[].tok_end is advanced by the merge kernel.
+  // Fused tail append (kf_decode_step; all NULL otherwise): the route that is
+  // its sequence's tail takes the step's token into its pages and attends
+  // over it; routes[].tok_end is advanced by the merge kernel.
   const uint16_t* k_new;       // [num_seqs][Hkv][kDim]
   const uint16_t* v_new;
   const int32_t* tail_route;   // [num_seqs]
-  uint16_t* k_pool_w;          // the pools, writable
-  uint16_t* v_pool_w;
+  void* k_pool_w;              // the pools, writable
+  void* v_pool_w;
+  float* k_scale_w;            // fp8 pools: the scales, writable
+  float* v_scale_w;
 };
 
 struct MergeArgs {

@@ -118,6 +118,47 @@ __device__ __forceinline__ float e4m3_value(uint32_t code) {
   return __builtin_bit_cast(float, b2 << 16);
 }
 
+// The E4M3 append rule for one token of one (page, KV head) of K (is_v
+// false, page [slot][d]) or V (page [d][slot]), by one wave whose lane holds
+// dims 2 lane, 2 lane + 1; all arithmetic in float32.  The first token of a
+// page sets scale = amax/28 (16x headroom below 448); a later token with
+// amax > 448*scale first re-encodes the page's earlier slots to amax/28; the
+// token is stored as RNE(x/scale).  Returns the page's scale afterwards
+// (old_scale is ignored for slot 0); the caller stores it.
+__device__ float append_e4m3_head(uint8_t* page, float old_scale, int slot, bool is_v,
+                                  const uint16_t* x_bits, int lane) {
+  const int d0 = 2 * lane;
+  const float x0 = __builtin_bit_cast(float, (uint32_t)x_bits[d0] << 16);
+  const float x1 = __builtin_bit_cast(float, (uint32_t)x_bits[d0 + 1] << 16);
+  float amax = fmaxf(fabsf(x0), fabsf(x1));
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) amax = fmaxf(amax, __shfl_xor(amax, m));
+  auto at = [&](int s_, int d_) -> uint8_t* {
+    return page + (is_v ? d_ * kPage + s_ : s_ * kDim + d_);
+  };
+  float scale;
+  if (slot == 0) {
+    scale = amax > 0.0f ? amax / 28.0f : 1.0f;
+  } else {
+    scale = old_scale;
+    if (amax > 448.0f * scale) {
+      const float fresh = amax / 28.0f;
+      for (int s_ = 0; s_ < slot; ++s_) {
+        uint8_t* p0 = at(s_, d0);
+        uint8_t* p1 = at(s_, d0 + 1);
+        const float v0 = e4m3_value(*p0) * scale;
+        const float v1 = e4m3_value(*p1) * scale;
+        *p0 = (uint8_t)e4m3_rne(v0 / fresh);
+        *p1 = (uint8_t)e4m3_rne(v1 / fresh);
+      }
+      scale = fresh;
+    }
+  }
+  *at(slot, d0) = (uint8_t)e4m3_rne(x0 / scale);
+  *at(slot, d0 + 1) = (uint8_t)e4m3_rne(x1 / scale);
+  return scale;
+}
+
 template <bool FP8>
 __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
   const int b = blockIdx.x;
@@ -160,50 +201,18 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
       vp[(head * kDim + d) * kPage + slot] = vv;
     }
   } else {
-    // One wave per (KV head, K|V); lane l holds dims 2l, 2l+1.  Page scales
-    // follow the E4M3 append rule: the first token of a page sets
-    // scale = amax/28 (16x headroom below 448); a later token with
-    // amax > 448*scale re-encodes the page's earlier slots to amax/28 first;
-    // the token is stored as RNE(x/scale).  All arithmetic in float32.
+    // One wave per (KV head, K|V)
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
-    const int d0 = 2 * lane;
     for (int pr = w; pr < 2 * H; pr += nw) {
       const int g = pr >> 1;
       const bool is_v = pr & 1;
-      const uint16_t* src = (is_v ? a.v_new : a.k_new) + ((size_t)b * H + g) * kDim + d0;
-      const float x0 = __builtin_bit_cast(float, (uint32_t)src[0] << 16);
-      const float x1 = __builtin_bit_cast(float, (uint32_t)src[1] << 16);
-      float amax = fmaxf(fabsf(x0), fabsf(x1));
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) amax = fmaxf(amax, __shfl_xor(amax, m));
-      float* scales = is_v ? a.v_scale : a.k_scale;
+      float* scale = (is_v ? a.v_scale : a.k_scale) + (size_t)pid * H + g;
       uint8_t* page = static_cast<uint8_t*>(is_v ? a.v_pool : a.k_pool) +
                       ((size_t)pid * H + g) * (kPage * kDim);
-      // element (slot s, dim d): K page [s][d], V page [d][s]
-      auto at = [&](int s_, int d_) -> uint8_t* {
-        return page + (is_v ? d_ * kPage + s_ : s_ * kDim + d_);
-      };
-      float scale;
-      if (slot == 0) {
-        scale = amax > 0.0f ? amax / 28.0f : 1.0f;
-      } else {
-        scale = scales[(size_t)pid * H + g];
-        if (amax > 448.0f * scale) {
-          const float fresh = amax / 28.0f;
-          for (int s_ = 0; s_ < slot; ++s_) {
-            uint8_t* p0 = at(s_, d0);
-            uint8_t* p1 = at(s_, d0 + 1);
-            const float v0 = e4m3_value(*p0) * scale;
-            const float v1 = e4m3_value(*p1) * scale;
-            *p0 = (uint8_t)e4m3_rne(v0 / fresh);
-            *p1 = (uint8_t)e4m3_rne(v1 / fresh);
-          }
-          scale = fresh;
-        }
-      }
-      if (lane == 0) scales[(size_t)pid * H + g] = scale;
-      *at(slot, d0) = (uint8_t)e4m3_rne(x0 / scale);
-      *at(slot, d0 + 1) = (uint8_t)e4m3_rne(x1 / scale);
+      const float s_new = append_e4m3_head(page, *scale, slot, is_v,
+                                           (is_v ? a.v_new : a.k_new) + ((size_t)b * H + g) * kDim,
+                                           lane);
+      if (lane == 0) *scale = s_new;
     }
   }
   __syncthreads();  // every thread has read tok_end before it moves
@@ -253,16 +262,35 @@ __device__ __forceinline__ RouteView read_route(const PartialArgs& a, int r) {
 
 // Fused step: write the step's token of KV head g into the route's page,
 // then make it visible to every wave of this workgroup before any of them
-// loads the page (waves of a workgroup share the compute unit's L1).
+// loads the page (waves of a workgroup share the compute unit's L1).  fp8
+// pools follow the E4M3 append rule (waves 0 and 1 take K and V) and hand
+// the page's new scales to the workgroup in s_app[0..1]: the scalar cache is
+// not coherent with vector stores, so the tail page's scales must not be
+// read back through scalar loads in this launch.
+template <bool FP8>
 __device__ __forceinline__ void write_new_token(const PartialArgs& a, const RouteView& rv, int g,
-                                                int tid) {
+                                                int tid, float* s_app) {
   const int H = a.num_kv_heads;
   const uint16_t* kn = a.k_new + ((size_t)rv.seq * H + g) * kDim;
   const uint16_t* vn = a.v_new + ((size_t)rv.seq * H + g) * kDim;
   const size_t head = (size_t)rv.app_pid * H + g;
-  if (tid < kDim) {
-    a.k_pool_w[(head * kPage + rv.app_slot) * kDim + tid] = kn[tid];
-    a.v_pool_w[(head * kDim + tid) * kPage + rv.app_slot] = vn[tid];
+  if constexpr (!FP8) {
+    if (tid < kDim) {
+      static_cast<uint16_t*>(a.k_pool_w)[(head * kPage + rv.app_slot) * kDim + tid] = kn[tid];
+      static_cast<uint16_t*>(a.v_pool_w)[(head * kDim + tid) * kPage + rv.app_slot] = vn[tid];
+    }
+  } else {
+    const int wv = tid >> 6, lane = tid & 63;
+    if (wv < 2) {
+      const bool is_v = wv == 1;
+      float* scale = (is_v ? a.v_scale_w : a.k_scale_w) + head;
+      uint8_t* page = static_cast<uint8_t*>(is_v ? a.v_pool_w : a.k_pool_w) + head * (kPage * kDim);
+      const float s_new = append_e4m3_head(page, *scale, rv.app_slot, is_v, is_v ? vn : kn, lane);
+      if (lane == 0) {
+        *scale = s_new;
+        s_app[wv] = s_new;
+      }
+    }
   }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
   __syncthreads();
@@ -324,6 +352,7 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
   __shared__ float s_l[kWaves][KF_MAX_GROUP];
   __shared__ float s_fm[KF_MAX_GROUP];
   __shared__ float s_fl[KF_MAX_GROUP];
+  __shared__ float s_app[2];  // fused fp8 append: the tail page's new K and V scales
 
   const int c = blockIdx.x;
   int g = blockIdx.y, u = blockIdx.z;  // u: position in the launch
@@ -353,8 +382,7 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
   const RouteView rv = read_route(a, r);
   if (rv.bad || rv.npages == 0) {
     if (c == 0) {
-      if constexpr (!FP8)
-        if (rv.app) write_new_token(a, rv, g, tid);  // the pool takes the token all the same
+      if (rv.app) write_new_token<FP8>(a, rv, g, tid, s_app);  // the pool takes the token all the same
       const float ov = rv.bad ? qnan() : 0.0f, lv = rv.bad ? qnan() : neg_inf();
       for (int e = tid; e < G * kDim; e += kThreads)
         a.o_part[((size_t)r * Hq + hq0 + e / kDim) * kDim + e % kDim] = ov;
@@ -366,8 +394,9 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
   const int seq = rv.seq, n = rv.n, npages = rv.npages;
   const int nchunks = (npages + a.chunk_pages - 1) / a.chunk_pages;
   if (c >= nchunks) return;
-  if constexpr (!FP8)
-    if (rv.app && c == nchunks - 1) write_new_token(a, rv, g, tid);  // the chunk with the last page
+  const bool writer = rv.app && c == nchunks - 1;  // the chunk with the last page
+  if (writer) write_new_token<FP8>(a, rv, g, tid, s_app);
+  const int app_page = (rv.n - 1) >> 4;             // route-local page of the new token
   const int p0 = (int)((int64_t)c * npages / nchunks);
   const int p1 = (int)((int64_t)(c + 1) * npages / nchunks);
   const int ntiles = (p1 - p0 + TP - 1) / TP;
@@ -407,6 +436,13 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
       t.vs1 = a.v_scale[(size_t)t.pid1 * H + g];
       t.vs2 = a.v_scale[(size_t)t.pid2 * H + g];
       t.vs3 = a.v_scale[(size_t)t.pid3 * H + g];
+      if (writer) {  // the tail page's scales were just written: take them from LDS
+        const int k = app_page - t.tp0;
+        if (k == 0) { t.ks0 = s_app[0]; t.vs0 = s_app[1]; }
+        if (k == 1) { t.ks1 = s_app[0]; t.vs1 = s_app[1]; }
+        if (k == 2) { t.ks2 = s_app[0]; t.vs2 = s_app[1]; }
+        if (k == 3) { t.ks3 = s_app[0]; t.vs3 = s_app[1]; }
+      }
     }
     return t;
   };

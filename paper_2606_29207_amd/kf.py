@@ -262,7 +262,7 @@ def decode_step(shape: Shape, q, k_pool, v_pool, k_new, v_new, routes, tail_rout
                 max_pages_per_route, page_ids, seq_route_begin, o_part, lse_part, out, lse_out,
                 workspace, err_flags, k_scale=None, v_scale=None, stream=None):
     """kf_decode_step: append -> partial attention -> merge in one call (two
-    launches for bf16 pools).  Arguments as for kv_append, partial_attn and
+    launches).  Arguments as for kv_append, partial_attn and
     merge_partials."""
     lib = load()
     for t, n in ((q, "q"), (k_pool, "k_pool"), (v_pool, "v_pool"), (k_new, "k_new"),

@@ -94,7 +94,7 @@ class DecodeState:
 
     def step_fused(self, k_new: torch.Tensor, v_new: torch.Tensor, stream=None):
         """One decode step through kf_decode_step: same results as step(),
-        with the append fused into the partial-attention launch (bf16)."""
+        with the append fused into the partial-attention launch."""
         kf.decode_step(self.shape, self.q, self.k_pool, self.v_pool, k_new, v_new, self.routes,
                        self.tail_route, self.max_pages_per_route, self.page_ids,
                        self.seq_route_begin, self.o_part, self.lse_part, self.out, self.lse,

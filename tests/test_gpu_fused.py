@@ -1,4 +1,4 @@
-"""kf_decode_step (append fused into partial attention for bf16 pools) on the
+"""kf_decode_step (append fused into partial attention) on the
 GPU: against the oracle at the usual bars, and bit for bit against the
 three separate calls on the same inputs, including every error path of the
 append."""
@@ -161,3 +161,25 @@ def test_fused_tail_crossing_max_pages(gpu):
     assert f0 == 0 and f1 | f2 == oracle.EFLAG_BAD_ROUTE
     compare_all(outs[1], dict(k_pool=kp, v_pool=vp, k_scale=None, v_scale=None, routes=rt,
                               o_part=o_part, lse_part=lse_part, out=out, lse=lse, flags=f1 | f2))
+
+
+def test_fused_fp8_reencode_of_pages_begun_by_appends(gpu):
+    """E4M3 pools through kf_decode_step with one step's tokens 100x larger:
+    the tail workgroups re-encode their pages and attend with the new scales
+    (passed through LDS), bit for bit as the three calls."""
+    from kf_workloads import bf16_bits_to_f32, f32_to_bf16_bits
+    wl = workload("wide_gqa_fp8", num_seqs=3, part_tokens=1024, appends=1)
+    inst = make_instance(wl, seed=5, steps=24, seq_lens=[3000, 2048, 1111])
+
+    def tokens(s):
+        kn, vn = inst.new_tokens(s)
+        if s != 12:
+            return kn, vn
+        up = lambda t: f32_to_bf16_bits(bf16_bits_to_f32(t) * np.float32(100.0))  # noqa: E731
+        return up(kn), up(vn)
+
+    f = host(run_gpu(inst, 24, new_tokens=tokens, fused=True))
+    same_bits(f, host(run_gpu(inst, 24, new_tokens=tokens)))
+    o = run_oracle(inst, 24, new_tokens=tokens)
+    for key in ("routes", "k_pool", "v_pool", "k_scale", "v_scale"):
+        assert np.array_equal(f[key], o[key]), key
