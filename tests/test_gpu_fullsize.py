@@ -1,6 +1,7 @@
 """Parity at the workloads' full sizes, in the launch configuration bench.py
-times (one decode step: append if the workload appends, partial attention,
-merge), on outputs the oracle can compute one unit at a time.
+times (one decode step of its default schedule: kf_decode_step when the
+workload appends, partial attention and merge when it does not), on outputs
+the oracle can compute one unit at a time.
 
 Per workload:
 * sampled (route, KV head) partials and sampled merged (sequence, KV group)
@@ -60,7 +61,7 @@ def test_fullsize_sampled(gpu, name):
         t.fill_(float("nan"))
     if wl.appends:
         kn, vn = inst.new_tokens(0)
-        st.step(*st.upload_new_tokens(kn, vn))
+        st.step_fused(*st.upload_new_tokens(kn, vn))
     else:
         st.step()
     torch.cuda.synchronize()
