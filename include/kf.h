@@ -84,7 +84,7 @@ typedef struct {
 enum {
   KF_OK = 0,
   KF_ERR_INVALID_ARG = -1, /* null/misaligned pointer or inconsistent sizes */
-  KF_ERR_UNSUPPORTED = -2, /* a shape or dtype this build does not handle */
+  KF_ERR_UNSUPPORTED = -2, /* a shape or dtype the library does not handle */
   KF_ERR_WORKSPACE = -3,   /* workspace missing or smaller than required */
   KF_ERR_HIP = -4,         /* the HIP runtime refused a launch */
   KF_ERR_CAPACITY = -5,    /* a caller-sized host output array is too small */

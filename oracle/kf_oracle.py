@@ -239,7 +239,7 @@ def kv_append(k_pool, v_pool, routes, page_ids, tail_route, k_new, v_new,
     tail (no reserved page for j) or an inconsistent route leaves that
     sequence unchanged and sets a flag.
 
-    E4M3 pools (no fp8 KV in the paper; this build's reading), per page and KV
+    E4M3 pools (no fp8 KV in the paper; the rule the kernels share), per page and KV
     head, separately for K and V, in float32 arithmetic:
       * the first token of a page sets scale = amax/28 (1 if amax = 0): its
         largest element lands at 28 = 448/16, leaving 16x headroom, which
