@@ -206,3 +206,27 @@ def test_debug_gather_host_checks(lib):
     assert call(out=None) == -1          # outputs needed when max_tokens > 0
     assert call(out=FAKE + 2) == -1      # misaligned
     assert call(max_tokens=0, out=None) == 0   # nothing to gather: no launch
+
+
+def test_binding_refuses_host_tensors_and_bad_shapes(lib):
+    """The binding fails loudly before any call: host (CPU) tensors where the
+    library needs device memory, and mismatched shapes."""
+    import torch
+    s = _shape(num_seqs=1, num_q_heads=8, num_kv_heads=2, num_pages=4, num_page_ids=4)
+    q = torch.zeros(1, 8, 128, dtype=torch.bfloat16)
+    pool = torch.zeros(4, 2, 16, 128, dtype=torch.bfloat16)
+    routes = torch.zeros(1, 6, dtype=torch.int32)
+    pids = torch.zeros(4, dtype=torch.int32)
+    o = torch.zeros(1, 8, 128)
+    lse = torch.zeros(1, 8)
+    ws = torch.zeros(256, dtype=torch.uint8)
+    flags = torch.zeros(1, dtype=torch.int32)
+    with pytest.raises(kf.KFError, match="device tensor"):
+        kf.partial_attn(s, q, pool, pool, routes, 1, pids, o, lse, ws, flags)
+    with pytest.raises(kf.KFError, match="device tensor"):
+        kf.kv_append(s, pool, pool, q[:, :2], q[:, :2], routes, flags, pids, flags)
+    with pytest.raises(kf.KFError, match="device tensor"):
+        kf.merge_partials(1, o, lse, torch.zeros(2, dtype=torch.int32), o, lse, flags)
+    with pytest.raises(kf.KFError, match="device tensor"):
+        kf.decode_step(s, q, pool, pool, q[:, :2], q[:, :2], routes, flags, 1, pids,
+                       torch.zeros(2, dtype=torch.int32), o, lse, o, lse, ws, flags)
