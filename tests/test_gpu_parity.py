@@ -32,6 +32,10 @@ CASES = {
     "fp8_append": ("wide_gqa_fp8", dict(num_seqs=3, part_tokens=1024, appends=1),
                    [3000, 2048, 1111], 20),
     "mha_g1": ("llama8b_32k", dict(num_seqs=2, num_q_heads=8, num_kv_heads=8, part_tokens=512), [900, 77], 1),
+    # E4M3 pools at other group sizes (the wide-GQA workload is G = 8)
+    "fp8_g1": ("wide_gqa_fp8", dict(num_seqs=2, num_q_heads=4, num_kv_heads=4, part_tokens=1024), [2100, 333], 1),
+    "fp8_g4": ("wide_gqa_fp8", dict(num_seqs=2, num_q_heads=16, num_kv_heads=4, part_tokens=768), [1600, 1025], 1),
+    "fp8_g16": ("wide_gqa_fp8", dict(num_seqs=2, num_q_heads=32, num_kv_heads=2, part_tokens=1024), [2500, 64], 1),
     "g16": ("llama8b_32k", dict(num_seqs=2, num_q_heads=32, num_kv_heads=2, part_tokens=1000), [1500, 2100], 1),
     "g8_bf16": ("llama8b_32k", dict(num_seqs=2, num_q_heads=64, num_kv_heads=8, part_tokens=700), [1400, 333], 1),
     # >= 512 (route, KV head) units: one workgroup per unit, no split
