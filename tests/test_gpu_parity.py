@@ -36,6 +36,9 @@ CASES = {
     "fp8_g1": ("wide_gqa_fp8", dict(num_seqs=2, num_q_heads=4, num_kv_heads=4, part_tokens=1024), [2100, 333], 1),
     "fp8_g4": ("wide_gqa_fp8", dict(num_seqs=2, num_q_heads=16, num_kv_heads=4, part_tokens=768), [1600, 1025], 1),
     "fp8_g16": ("wide_gqa_fp8", dict(num_seqs=2, num_q_heads=32, num_kv_heads=2, part_tokens=1024), [2500, 64], 1),
+    # group sizes that are not powers of two
+    "g3_bf16": ("llama8b_32k", dict(num_seqs=2, num_q_heads=6, num_kv_heads=2, part_tokens=600), [1300, 601], 1),
+    "fp8_g12": ("wide_gqa_fp8", dict(num_seqs=2, num_q_heads=24, num_kv_heads=2, part_tokens=1024), [1800, 900], 1),
     "g16": ("llama8b_32k", dict(num_seqs=2, num_q_heads=32, num_kv_heads=2, part_tokens=1000), [1500, 2100], 1),
     "g8_bf16": ("llama8b_32k", dict(num_seqs=2, num_q_heads=64, num_kv_heads=8, part_tokens=700), [1400, 333], 1),
     # >= 512 (route, KV head) units: one workgroup per unit, no split
