@@ -17,8 +17,8 @@ Source: KernelFlume (arXiv 2606.29207).
 * Section 4.2 (Elastic Scaling Policy), post-prefill initialisation and
   Algorithm 1: KV footprint C_total = sum_i 2 s_i H_kv d_h L * 2 B.
 
-Readings where the paper is silent (the kernels take the same ones):
-notes): a partial is exported as (normalised o, lse = m + ln l) instead of
+Readings where the paper is silent (the kernels take the same ones): a
+partial is exported as (normalised o, lse = m + ln l) instead of
 (unnormalised o, m, l); the softmax scale is 1/sqrt(d) applied to the fp64
 score; query head h reads KV head h // (H_q / H_kv); the tail attends to the
 token it has just appended; an empty range gives (o = 0, lse = -inf).
