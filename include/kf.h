@@ -88,7 +88,8 @@ enum {
   KF_ERR_WORKSPACE = -3,   /* workspace missing or smaller than required */
   KF_ERR_HIP = -4,         /* the HIP runtime refused a launch */
   KF_ERR_CAPACITY = -5,    /* a caller-sized host output array is too small */
-  KF_ERR_INFEASIBLE = -6   /* no budget satisfies the constraints */
+  KF_ERR_INFEASIBLE = -6,  /* no budget satisfies the constraints */
+  KF_ERR_HOST_MEMORY = -7  /* host-side temporaries could not be allocated */
 };
 
 enum { KF_KV_BF16 = 0, KF_KV_FP8_E4M3 = 1 };

@@ -12,7 +12,9 @@
  * call is synchronous, nothing is allocated that outlives a call, and no GPU
  * is touched.  Invalid arguments return KF_ERR_INVALID_ARG before any output
  * is written; an output array that is too small returns KF_ERR_CAPACITY
- * with nothing modified (the required counts are reported where stated).
+ * with nothing modified (the required counts are reported where stated); a
+ * failure to allocate host temporaries returns KF_ERR_HOST_MEMORY (no
+ * exception leaves the library).
  *
  * Readings where the paper leaves a choice
  * ----------------------------------------

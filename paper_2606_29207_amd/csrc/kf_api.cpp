@@ -102,6 +102,7 @@ const char* kf_status_str(int status) {
     case KF_ERR_HIP: return "HIP runtime error";
     case KF_ERR_CAPACITY: return "output array too small";
     case KF_ERR_INFEASIBLE: return "infeasible budget";
+    case KF_ERR_HOST_MEMORY: return "host memory exhausted";
     default: return "unknown status";
   }
 }

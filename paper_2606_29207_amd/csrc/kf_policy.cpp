@@ -159,7 +159,7 @@ int kf_policy_init(const kf_policy_params* p, const int64_t* seq_lens, int32_t n
   return KF_OK;
 }
 
-int kf_policy_monitor(const kf_policy_params* p, int64_t step, int32_t num_seqs,
+static int kf_policy_monitor_impl(const kf_policy_params* p, int64_t step, int32_t num_seqs,
                       const uint8_t* active, const int64_t* seq_len, int32_t* tail,
                       kf_policy_node* nodes, int32_t* num_nodes, int32_t max_nodes,
                       kf_policy_range* ranges, int32_t* num_ranges, int32_t max_ranges,
@@ -240,7 +240,7 @@ int kf_policy_monitor(const kf_policy_params* p, int64_t step, int32_t num_seqs,
   return KF_OK;
 }
 
-int kf_policy_simulate(const kf_policy_params* p, const int64_t* seq_lens,
+static int kf_policy_simulate_impl(const kf_policy_params* p, const int64_t* seq_lens,
                        const int64_t* gen_lens, int32_t num_seqs, int64_t steps,
                        int32_t max_nodes, int32_t max_ranges, int32_t max_events,
                        int32_t* tails_per_step, kf_policy_node* nodes, int32_t* num_nodes,
@@ -300,7 +300,7 @@ int kf_policy_simulate(const kf_policy_params* p, const int64_t* seq_lens,
   return KF_OK;
 }
 
-int kf_policy_build_routes(const kf_policy_range* ranges, int32_t num_ranges,
+static int kf_policy_build_routes_impl(const kf_policy_range* ranges, int32_t num_ranges,
                            int32_t num_seqs, const int64_t* seq_len_now, int32_t page_size,
                            const int32_t* free_pages, int32_t num_free, kf_route* routes,
                            int32_t* seq_route_begin, int32_t* range_to_route,
@@ -343,6 +343,44 @@ int kf_policy_build_routes(const kf_policy_range* ranges, int32_t num_ranges,
   }
   for (int32_t i = 0; i < num_seqs; ++i) seq_route_begin[i + 1] += seq_route_begin[i];
   return KF_OK;
+}
+
+int kf_policy_monitor(const kf_policy_params* p, int64_t step, int32_t num_seqs,
+                      const uint8_t* active, const int64_t* seq_len, int32_t* tail,
+                      kf_policy_node* nodes, int32_t* num_nodes, int32_t max_nodes,
+                      kf_policy_range* ranges, int32_t* num_ranges, int32_t max_ranges,
+                      kf_policy_event* events, int32_t* num_events, int32_t max_events) {
+  try {
+    return kf_policy_monitor_impl(p, step, num_seqs, active, seq_len, tail, nodes, num_nodes, max_nodes, ranges, num_ranges, max_ranges, events, num_events, max_events);
+  } catch (...) {  // host temporaries could not be allocated: no exception crosses the C ABI
+    return KF_ERR_HOST_MEMORY;
+  }
+}
+
+int kf_policy_simulate(const kf_policy_params* p, const int64_t* seq_lens,
+                       const int64_t* gen_lens, int32_t num_seqs, int64_t steps,
+                       int32_t max_nodes, int32_t max_ranges, int32_t max_events,
+                       int32_t* tails_per_step, kf_policy_node* nodes, int32_t* num_nodes,
+                       kf_policy_range* ranges, int32_t* num_ranges, int32_t* tail,
+                       kf_policy_event* events, int32_t* num_events, int64_t* seq_len_out,
+                       int64_t* max_node_bytes) {
+  try {
+    return kf_policy_simulate_impl(p, seq_lens, gen_lens, num_seqs, steps, max_nodes, max_ranges, max_events, tails_per_step, nodes, num_nodes, ranges, num_ranges, tail, events, num_events, seq_len_out, max_node_bytes);
+  } catch (...) {  // host temporaries could not be allocated: no exception crosses the C ABI
+    return KF_ERR_HOST_MEMORY;
+  }
+}
+
+int kf_policy_build_routes(const kf_policy_range* ranges, int32_t num_ranges,
+                           int32_t num_seqs, const int64_t* seq_len_now, int32_t page_size,
+                           const int32_t* free_pages, int32_t num_free, kf_route* routes,
+                           int32_t* seq_route_begin, int32_t* range_to_route,
+                           int32_t* page_ids, int32_t max_page_ids, int32_t* num_page_ids) {
+  try {
+    return kf_policy_build_routes_impl(ranges, num_ranges, num_seqs, seq_len_now, page_size, free_pages, num_free, routes, seq_route_begin, range_to_route, page_ids, max_page_ids, num_page_ids);
+  } catch (...) {  // host temporaries could not be allocated: no exception crosses the C ABI
+    return KF_ERR_HOST_MEMORY;
+  }
 }
 
 }  // extern "C"

@@ -26,6 +26,7 @@ ERR_WORKSPACE = -3
 ERR_HIP = -4
 ERR_CAPACITY = -5
 ERR_INFEASIBLE = -6
+ERR_HOST_MEMORY = -7
 
 EFLAG_TAIL_FULL = 1
 EFLAG_BAD_ROUTE = 2

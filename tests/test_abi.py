@@ -51,7 +51,8 @@ def test_struct_layouts_match_header():
 
 def test_status_strings(lib):
     for code, text in ((0, "ok"), (-1, "invalid argument"), (-2, "unsupported"),
-                       (-3, "workspace"), (-4, "HIP"), (-5, "too small"), (-6, "infeasible")):
+                       (-3, "workspace"), (-4, "HIP"), (-5, "too small"), (-6, "infeasible"),
+                       (-7, "host memory")):
         assert text in kf.status_str(code)
     assert kf.status_str(12345) == "unknown status"
 
