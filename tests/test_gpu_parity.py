@@ -287,3 +287,44 @@ def test_subset_writes_only_listed_rows_and_flags_bad_entries(gpu):
     assert_close_o(o[listed], ref_o[listed], "o_part listed")
     assert_close_lse(lse[listed], ref_l[listed], "lse_part listed")
     assert np.all(o[others] == 7.0) and np.all(lse[others] == 7.0)
+
+
+@pytest.mark.parametrize("case", ["tiny_append", "llama_ragged", "agentic_small", "million_small",
+                                  "wide_fp8_small", "fp8_append"])
+def test_config_shapes_second_seed(gpu, case):
+    """Every workload shape at a second seed (parity runs seeds 1 and 2)."""
+    name, over, lens, steps = CASES[case]
+    inst = make_instance(workload(name, **over), seed=2, steps=steps, seq_lens=lens)
+    compare_all(host(run_gpu(inst, steps)), run_oracle(inst, steps))
+
+
+def test_scale_down_drops_a_finished_request(gpu):
+    """Between steps the host drops the routes of a finished request (the
+    scale-down of Section 4.2: a node retires once its requests complete).
+    The next step leaves the other requests exactly as the oracle on the new
+    table, and the dropped request merges to (0, -inf)."""
+    import torch
+    from paper_2606_29207_amd.step import DecodeState
+    wl = workload("llama8b_32k", num_seqs=3, num_q_heads=8, num_kv_heads=2, part_tokens=700)
+    inst = make_instance(wl, seed=6, steps=2, seq_lens=[1500, 2222, 901])
+    st = run_gpu(inst, 1)
+    g0 = host(st)
+    keep = [r for r in range(len(g0["routes"])) if g0["routes"][r, 0] != 1]
+    routes = g0["routes"][keep]
+    srb = np.array([0] + [int((routes[:, 0] <= b).sum()) for b in range(3)], np.int32)
+    tail = np.array([keep.index(t) if t in keep else -1 for t in inst.tail_route], np.int32)
+    st2 = DecodeState(q=inst.q, k_pool=g0["k_pool"], v_pool=g0["v_pool"], routes=routes,
+                      page_ids=inst.page_ids, seq_route_begin=srb, tail_route=tail,
+                      scale=inst.scale, max_pages_per_route=inst.max_pages_per_route)
+    kn, vn = inst.new_tokens(1)
+    st2.step_fused(*st2.upload_new_tokens(kn, vn))
+    torch.cuda.synchronize()
+    g = host(st2)
+    kp, vp, rt, f0 = oracle.kv_append(g0["k_pool"], g0["v_pool"], routes, inst.page_ids, tail, kn, vn)
+    o_part, lse_part, f1 = oracle.partial_attn(inst.q, kp, vp, rt, inst.page_ids, num_kv_heads=2,
+                                               scale=inst.scale,
+                                               max_pages_per_route=inst.max_pages_per_route)
+    out, lse, f2 = oracle.merge_partials(o_part, lse_part, srb)
+    compare_all(g, dict(k_pool=kp, v_pool=vp, k_scale=None, v_scale=None, routes=rt, o_part=o_part,
+                        lse_part=lse_part, out=out, lse=lse, flags=f0 | f1 | f2))
+    assert np.all(g["out"][1] == 0) and np.all(np.isneginf(g["lse"][1]))
