@@ -95,6 +95,7 @@ def _partial(lib, shape, **kw):
     ({"num_pages": 0}, {}, -1),
     ({"scale": float("nan")}, {}, -1),
     ({}, dict(R=-1), -1),
+    ({}, dict(R=65536), -2),                         # launch grid: at most 65535 routes
     ({}, dict(R=70000), -2),
 ])
 def test_partial_attn_host_checks(lib, shape_kw, call_kw, status):

@@ -1,6 +1,7 @@
 """Degenerate and extreme shapes on the GPU against the oracle: a sequence
 cut into thousands of 1-17 token routes (merge fan-in in the thousands),
-beside a sequence with a few long routes and one with no tokens."""
+beside a sequence with a few long routes and one with no tokens; and the
+largest route count one launch takes."""
 import numpy as np
 import pytest
 
@@ -49,3 +50,24 @@ def test_thousands_of_tiny_routes(gpu):
     assert np.abs(g["out"][0] - ref_o).max() <= 2e-3
     assert np.abs(g["lse"][0] - ref_l).max() <= 1e-4
     assert np.all(g["out"][2] == 0) and np.all(np.isneginf(g["lse"][2]))   # no tokens
+
+
+def test_route_count_limit(gpu):
+    """65535 routes, the most one launch takes (its grid's z extent): one
+    sequence cut into 65534 routes of 1-4 tokens (merge fan-in 65534) beside
+    a one-route sequence; 65536 routes are refused on the host."""
+    rng = np.random.default_rng(5)
+    lens = [int(x) for x in rng.integers(1, 5, 65534)]
+    routes, page_ids, srb, tails, n0 = tiny_route_table(lens, [37])
+    wl = workload("llama8b_32k", num_seqs=2, num_q_heads=4, num_kv_heads=1, part_tokens=1 << 20)
+    inst = make_instance(wl, seed=11, seq_lens=[n0, 37], routing=(routes, page_ids, srb, tails))
+    assert len(inst.routes) == 65535
+    o = run_oracle(inst, 1)
+    g = host(run_gpu(inst, 1))
+    compare_all(g, o)
+    q = bf16_bits_to_f32(inst.q).astype(np.float64)
+    K, V = inst.logical_kv(0, 0, n0)
+    ref_o, ref_l = oracle.attend(q[0], oracle.bf16_to_f64(K[:, 0]), oracle.bf16_to_f64(V[:, 0]),
+                                 inst.scale)
+    assert np.abs(g["out"][0] - ref_o).max() <= 2e-3
+    assert np.abs(g["lse"][0] - ref_l).max() <= 1e-4
