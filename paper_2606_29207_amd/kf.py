@@ -224,8 +224,9 @@ def partial_attn(shape: Shape, q, k_pool, v_pool, routes, max_pages_per_route, p
             _dev(t, n)
             _need(t.dtype == torch.float32 and t.numel() >= shape.num_pages * shape.num_kv_heads,
                   f"{n} must be float32 [num_pages, num_kv_heads]")
+    ws_bytes = workspace.numel() * workspace.element_size()
     common_tail = (int(max_pages_per_route), _ptr(page_ids), _ptr(o_part), _ptr(lse_part),
-                   _ptr(workspace), workspace.numel(), _ptr(err_flags), _stream(stream))
+                   _ptr(workspace), ws_bytes, _ptr(err_flags), _stream(stream))
     if route_list is None:
         st = lib.kf_partial_attn(ctypes.byref(shape), _ptr(q), _ptr(k_pool), _ptr(v_pool),
                                  _ptr(k_scale), _ptr(v_scale), _ptr(routes), R, *common_tail)
@@ -295,7 +296,8 @@ def decode_step(shape: Shape, q, k_pool, v_pool, k_new, v_new, routes, tail_rout
                             _ptr(v_scale), _ptr(k_new), _ptr(v_new), _ptr(routes), R,
                             _ptr(tail_route), int(max_pages_per_route), _ptr(page_ids),
                             _ptr(seq_route_begin), _ptr(o_part), _ptr(lse_part), _ptr(out),
-                            _ptr(lse_out), _ptr(workspace), workspace.numel(), _ptr(err_flags),
+                            _ptr(lse_out), _ptr(workspace),
+                            workspace.numel() * workspace.element_size(), _ptr(err_flags),
                             _stream(stream))
     _check(st, "kf_decode_step")
 
