@@ -8,8 +8,10 @@
 // head).  One 256-thread workgroup (four waves, two workgroups per CU) owns a
 // (route, KV head) unit -- or, when the host plans chunks, one of its
 // ceil(pages / chunk_pages) page ranges.  Wave w takes tiles w, w+4, ... of
-// the range, so the summation order is fixed and results are bitwise
-// reproducible.  Each wave streams tiles of 2 (bf16) or 4 (fp8) pages:
+// the range, its full tiles taken from a per-route starting offset, so the
+// summation order is fixed and results are bitwise reproducible (and the
+// same for any placement of the pages).  Each wave streams tiles of 2 (bf16)
+// or 4 (fp8) pages:
 //   * lane (grp = lane/16, i = lane%16).  For q.K^T the MFMA A operand row i
 //     is token (page i/4 of the tile, slot 4c + i%4) for c = 0..3, so the
 //     16x16 result lands with lane (grp, head i) holding all 16 scores of
@@ -402,6 +404,18 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
   const int ntiles = (p1 - p0 + TP - 1) / TP;
   const int lim = min(n, p1 * kPage);  // route-local token bound of this range
   const int32_t* __restrict__ pids = a.page_ids + rv.base;
+  // All workgroups start together and stream at about the same pace, so
+  // without care every route reads the same offset of its range at the same
+  // moment; in a contiguous pool that puts the routes of a sequence (equal
+  // sizes apart) on the same DRAM channels at once.  Each route therefore
+  // walks its full tiles starting from its own offset, rot (golden-ratio
+  // hash of the route index, the same for every KV head and chunk of the
+  // route, so the heads keep reading the same pages together).  A partial
+  // last tile keeps its place at the end and is computed masked.  The order
+  // depends on the route index only, never on page ids.
+  const int nfull = (lim == p1 * kPage && (p1 - p0) % TP == 0) ? ntiles : ntiles - 1;
+  const int rot =
+      nfull > 1 ? (int)(((uint64_t)((uint32_t)r * 2654435769u) * (uint32_t)nfull) >> 32) : 0;
 
   auto next_tile = [&](int cur) -> int { return cur + kWaves; };  // wave w: w, w+4, ...
 
@@ -421,7 +435,8 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
   };
   auto tile_info = [&](int tile) -> TileInfo {  // tile: index within the range
     TileInfo t;
-    t.tp0 = p0 + tile * TP;
+    const int tr = tile < nfull ? (tile + rot < nfull ? tile + rot : tile + rot - nfull) : tile;
+    t.tp0 = p0 + tr * TP;
     t.pid0 = page_at(t.tp0);
     t.pid1 = page_at(t.tp0 + 1);
     t.pid2 = TP > 2 ? page_at(t.tp0 + 2) : 0;
