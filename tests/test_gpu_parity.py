@@ -41,6 +41,11 @@ CASES = {
     "fp8_g12": ("wide_gqa_fp8", dict(num_seqs=2, num_q_heads=24, num_kv_heads=2, part_tokens=1024), [1800, 900], 1),
     "g16": ("llama8b_32k", dict(num_seqs=2, num_q_heads=32, num_kv_heads=2, part_tokens=1000), [1500, 2100], 1),
     "g8_bf16": ("llama8b_32k", dict(num_seqs=2, num_q_heads=64, num_kv_heads=8, part_tokens=700), [1400, 333], 1),
+    "g2_bf16": ("llama8b_32k", dict(num_seqs=2, num_q_heads=4, num_kv_heads=2, part_tokens=900), [1900, 450], 1),
+    "g5_bf16": ("llama8b_32k", dict(num_seqs=2, num_q_heads=10, num_kv_heads=2, part_tokens=800), [1700, 801], 1),
+    "fp8_g2": ("wide_gqa_fp8", dict(num_seqs=2, num_q_heads=8, num_kv_heads=4, part_tokens=1024), [2049, 700], 1),
+    # many KV heads (32), each with a group of 2
+    "hkv32_g2": ("llama8b_32k", dict(num_seqs=2, num_q_heads=64, num_kv_heads=32, part_tokens=1024), [1500, 530], 1),
     # >= 512 (route, KV head) units: one workgroup per unit, no split
     "many_units": ("llama8b_32k", dict(part_tokens=256), [300 + 97 * i for i in range(16)], 2),
     # > 512 units, not a whole number of rounds, uneven routes: chunked units
@@ -328,3 +333,37 @@ def test_scale_down_drops_a_finished_request(gpu):
     compare_all(g, dict(k_pool=kp, v_pool=vp, k_scale=None, v_scale=None, routes=rt, o_part=o_part,
                         lse_part=lse_part, out=out, lse=lse, flags=f0 | f1 | f2))
     assert np.all(g["out"][1] == 0) and np.all(np.isneginf(g["lse"][1]))
+
+
+def test_nan_inputs_poison_only_their_unit(gpu):
+    """A NaN in one resident K element makes the partial of that (route, KV
+    head) NaN in all of o and in lse; a NaN in one V element makes only that
+    dimension of its o NaN and leaves its lse finite; both reach their
+    sequence's merged output and nothing else, exactly as in the oracle
+    (equal NaN positions, the rest within tolerance, no error flag)."""
+    BF16_NAN = 0x7FC0
+    inst = make_instance(workload("llama8b_32k", num_seqs=3, num_q_heads=8, num_kv_heads=2,
+                                  part_tokens=1024), seed=4, seq_lens=[2500, 2100, 1500])
+    r_k, r_v = 0, 3          # route 0 (sequence 0), route 3 (sequence 1)
+    assert inst.routes[r_k, 0] == 0 and inst.routes[r_v, 0] == 1
+    pk = inst.page_ids[inst.routes[r_k, 4] + 1]          # local page 1, slot 5, head 0, dim 7
+    inst.k_pool[pk, 0, 5, 7] = BF16_NAN
+    pv = inst.page_ids[inst.routes[r_v, 4] + 2]          # local page 2, slot 9, head 1, dim 100
+    inst.v_pool[pv, 1, 100, 9] = BF16_NAN
+    o = run_oracle(inst, 1)
+    g = host(run_gpu(inst, 1))
+    compare_all(g, o)
+    G = 4
+    nan_o = np.isnan(g["o_part"]).any(axis=2)
+    nan_l = np.isnan(g["lse_part"])
+    want_o = np.zeros_like(nan_o)
+    want_o[r_k, 0:G] = True
+    want_o[r_v, G:2 * G] = True
+    want_l = np.zeros_like(nan_l)
+    want_l[r_k, 0:G] = True
+    assert np.array_equal(nan_o, want_o) and np.array_equal(nan_l, want_l)
+    assert np.isnan(g["out"][0, 0:G]).all() and np.isnan(g["lse"][0, 0:G]).all()
+    assert np.isnan(g["out"][1, G:2 * G, 100]).all() and np.isfinite(g["lse"][1]).all()
+    assert np.isnan(g["out"][1]).sum() == G and np.isnan(g["o_part"][r_v]).sum() == G
+    assert np.isnan(g["o_part"][r_k, 0:G]).all()
+    assert np.isfinite(g["out"][2]).all() and g["flags"] == 0
