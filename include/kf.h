@@ -131,8 +131,10 @@ int kf_kv_append(const kf_shape* shape, void* k_pool, void* v_pool, float* k_sca
  * current device (at least 256 bytes).  One workgroup handles a whole
  * (route, KV head) unit when there are enough units to fill the GPU; with
  * fewer, each unit is split over several workgroups whose partials go through
- * this workspace.  No initialisation is needed; contents are dead between
- * calls.  Returns 0 for invalid arguments.
+ * this workspace.  The size covers every launch of at most `num_routes`
+ * routes, so a workspace sized for a route table also serves
+ * kf_partial_attn_subset over any part of it.  No initialisation is needed;
+ * contents are dead between calls.  Returns 0 for invalid arguments.
  */
 size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes,
                                        int32_t max_pages_per_route);

@@ -113,8 +113,16 @@ size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes
                                        int32_t max_pages_per_route) {
   if (check_shape(shape) != KF_OK || num_routes < 0 || max_pages_per_route < 0) return 0;
   const int32_t group = shape->num_q_heads / shape->num_kv_heads;
-  const kf::ChunkPlan plan = kf::plan_chunks(num_routes, shape->num_kv_heads, max_pages_per_route);
-  return kf::workspace_layout(num_routes, shape->num_kv_heads, group, plan.max_chunks).total;
+  // The largest need of any launch of at most num_routes routes: fewer routes
+  // may not fill the GPU and then split their units, so a workspace sized for
+  // a whole route table must also serve a launch over a subset of it.
+  size_t most = 0;
+  for (int32_t m = num_routes > 0 ? 1 : 0; m <= num_routes; ++m) {
+    const kf::ChunkPlan plan = kf::plan_chunks(m, shape->num_kv_heads, max_pages_per_route);
+    const size_t t = kf::workspace_layout(m, shape->num_kv_heads, group, plan.max_chunks).total;
+    if (t > most) most = t;
+  }
+  return most;
 }
 
 }  // extern "C"

@@ -176,21 +176,42 @@ def test_merge_host_checks(lib):
     assert lib.kf_merge_partials(0, 4, 8, 128, *([None] * 7), None) == 0
 
 
-def test_workspace_bytes(lib):
-    """Enough (route, KV head) units to fill 256 CUs: no split, minimum size.
-    Four units of 128 pages: 8 splits of 16 pages, records of (o, max, sum)."""
+def _workspace_need(units_routes, H, G, maxp, slots=512):
+    """Bytes one launch of `units_routes` routes needs, by the planner's rule:
+    units that fill whole rounds of the resident slots stay whole (no
+    records); otherwise chunks of about one per slot (fewer units than
+    slots) or 32 per slot, never under 16 pages; records of (max, sum) and
+    o per query head, each array rounded up to 256 bytes."""
     rup = lambda x: -(-x // 256) * 256  # noqa: E731
+    units = units_routes * H
+    if units == 0 or maxp <= 16 or (units >= slots and units % slots == 0):
+        return 256
+    target = slots if units < slots else 32 * slots
+    c = max(-(-units * maxp // target), 16)
+    if c >= maxp:
+        return 256
+    recs = units * -(-maxp // c) * G
+    return rup(recs * 2 * 4) + rup(recs * 128 * 4)
+
+
+def test_workspace_bytes(lib):
+    """The size covers every launch of at most num_routes routes (a subset
+    launch of a table that fills the GPU may split its units)."""
     s = _shape(num_seqs=16, num_q_heads=32, num_kv_heads=8, num_pages=40000, num_page_ids=40000)
-    assert kf.partial_attn_workspace_bytes(s, 64, 513) == 256
+    sizes = [kf.partial_attn_workspace_bytes(s, m, 513) for m in range(0, 80)]
+    assert all(a <= b for a, b in zip(sizes, sizes[1:]))            # non-decreasing
+    for m in range(0, 80):
+        assert sizes[m] == max(_workspace_need(k, 8, 4, 513) for k in range(0, m + 1))
+    assert _workspace_need(64, 8, 4, 513) == 256                   # 512 units: one round, unsplit
+    assert sizes[64] == _workspace_need(63, 8, 4, 513) > 256         # ... but 63 routes split
+    # 1 sequence, 2 routes of 128 pages, 2 KV heads: 8 splits of 16 pages
     s = _shape(num_seqs=1, num_q_heads=8, num_kv_heads=2, num_pages=256, num_page_ids=256)
     recs = 2 * 2 * 8 * 4
-    assert kf.partial_attn_workspace_bytes(s, 2, 128) == rup(recs * 2 * 4) + rup(recs * 128 * 4)
-    # 142 routes x 8 KV heads of up to 1025 pages: 1136 units do not fill whole
-    # rounds of 512 resident workgroups -> chunks of ceil(1136*1025/16384) = 72
-    # pages, at most 15 per unit
+    assert kf.partial_attn_workspace_bytes(s, 2, 128) == 1024 + recs * 128 * 4
+    # 142 routes x 8 KV heads of up to 1025 pages
     s = _shape(num_seqs=64, num_q_heads=32, num_kv_heads=8, num_pages=10, num_page_ids=10)
-    recs = 142 * 8 * 15 * 4
-    assert kf.partial_attn_workspace_bytes(s, 142, 1025) == rup(recs * 2 * 4) + rup(recs * 128 * 4)
+    assert kf.partial_attn_workspace_bytes(s, 142, 1025) == max(
+        _workspace_need(k, 8, 4, 1025) for k in range(143))
     assert kf.partial_attn_workspace_bytes(s, -1, 5) == 0
     assert kf.partial_attn_workspace_bytes(_shape(head_dim=64), 4, 5) == 0
 

@@ -245,7 +245,7 @@ def test_split_invariance_against_one_route(gpu, parts):
 
 
 # ------------------------------------------------------------ query-first step
-@pytest.mark.parametrize("case", ["llama", "agentic"])
+@pytest.mark.parametrize("case", ["llama", "agentic", "table_fills_gpu"])
 def test_query_first_step_matches_oracle(gpu, case):
     """Section 5.1: historical partials from q alone on one stream, append +
     tail partials on another, merge after both; equal to the serial step."""
@@ -254,6 +254,13 @@ def test_query_first_step_matches_oracle(gpu, case):
     if case == "llama":
         inst = make_instance(workload("llama8b_32k", num_seqs=3, part_tokens=1024),
                              seed=11, steps=3, seq_lens=[3001, 1700, 4103])
+    elif case == "table_fills_gpu":
+        # 64 routes x 8 KV heads = 512 units: the whole table runs unsplit,
+        # the 48 historical routes alone are split and need chunk records
+        # (the workspace is sized once, for the whole table)
+        inst = make_instance(workload("llama8b_32k", part_tokens=512),
+                             seed=13, steps=3, seq_lens=[2048] * 16)
+        assert len(inst.routes) == 64
     else:
         inst = make_instance(workload("agentic_mix", num_seqs=5, ctx_range=(300, 5000),
                                       part_tokens=1024), seed=12, steps=3)
