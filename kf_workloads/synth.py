@@ -18,7 +18,8 @@ head_dim 128):
   at slot ``(t-tok_begin) % 16``.
 
 Unused slots of every page are filled with NaN bit patterns so that a reader
-that touches them shows it.
+that touches them shows it.  A contiguous pool hands out pages in pairs (each
+route starts on an even page id); a permuted pool is one random permutation.
 """
 from __future__ import annotations
 
@@ -273,9 +274,17 @@ def make_instance(wl: Workload, seed: int = 1, *, steps: int = 1,
         routes[:, 4] = np.concatenate([[0], np.cumsum(caps)[:-1]]).astype(np.int32)
         if wl.permuted:
             page_ids = _rng(seed, wl.wid, _T_PERM).permutation(total).astype(np.int32)
+            P = max(total, 1)
         else:
-            page_ids = np.arange(total, dtype=np.int32)
-        P = max(total, 1)
+            # contiguous pool, pages handed out in pairs (64 KiB of bf16 K per
+            # pair at 8 KV heads): each route's pages start on an even page id,
+            # a route reserving an odd count leaves one unused page behind it
+            even = caps + (caps & 1)
+            first = np.concatenate([[0], np.cumsum(even)[:-1]])
+            page_ids = np.concatenate(
+                [first[r] + np.arange(caps[r]) for r in range(len(caps))]
+            ).astype(np.int32) if len(caps) else np.zeros(0, np.int32)
+            P = max(int(even.sum()), 1)
 
     fp8 = wl.kv_dtype == "fp8"
     edt = np.uint8 if fp8 else np.uint16
