@@ -81,3 +81,23 @@ def test_unused_slots_hold_nan():
         assert np.all(inst.k_pool.transpose(0, 2, 1, 3)[free] == nan)
         assert np.all(inst.v_pool.transpose(0, 3, 1, 2)[free] == nan)
         assert not np.any(inst.k_pool.transpose(0, 2, 1, 3)[used] == nan)
+
+
+def test_contiguous_pool_hands_out_pages_in_pairs():
+    """Every route of a contiguous pool starts on an even page id, its pages
+    are consecutive, no page is shared, and capacities are as requested
+    (odd reservations leave one unused page behind them)."""
+    for steps in (1, 2, 65):
+        inst = make_instance(workload("llama8b_32k", num_seqs=3, part_tokens=1000), seed=2,
+                             steps=steps, seq_lens=[2100, 999, 3001])
+        seen = []
+        for r in inst.routes:
+            base, cap = int(r[4]), int(r[5])
+            ids = inst.page_ids[base:base + cap]
+            assert ids[0] % 2 == 0
+            assert np.array_equal(ids, ids[0] + np.arange(cap))
+            assert cap == -(-(int(r[3] - r[2]) + (steps if r[1] == inst.routes[
+                inst.seq_route_begin[r[0] + 1] - 1, 1] else 0)) // 16)
+            seen.append(ids)
+        seen = np.concatenate(seen)
+        assert len(np.unique(seen)) == len(seen) and seen.max() < inst.num_pages
