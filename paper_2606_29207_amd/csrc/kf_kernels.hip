@@ -406,13 +406,14 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
   const int32_t* __restrict__ pids = a.page_ids + rv.base;
   // All workgroups start together and stream at about the same pace, so
   // without care every route reads the same offset of its range at the same
-  // moment; in a contiguous pool that puts the routes of a sequence (equal
-  // sizes apart) on the same DRAM channels at once.  Each route therefore
-  // walks its full tiles starting from its own offset, rot (golden-ratio
-  // hash of the route index, the same for every KV head and chunk of the
-  // route, so the heads keep reading the same pages together).  A partial
-  // last tile keeps its place at the end and is computed masked.  The order
-  // depends on the route index only, never on page ids.
+  // moment, and in a contiguous pool (routes of a sequence equal sizes apart)
+  // the DRAM channels hit at each moment then depend on the pool's layout:
+  // the same work ran up to ~9% slower on some page reservations.  Each route
+  // therefore walks its full tiles starting from its own offset, rot (a
+  // golden-ratio hash of the route index, the same for every KV head and
+  // chunk of the route, so the heads keep reading the same pages together).
+  // A partial last tile keeps its place at the end and is computed masked.
+  // The order depends on the route index only, never on page ids.
   const int nfull = (lim == p1 * kPage && (p1 - p0) % TP == 0) ? ntiles : ntiles - 1;
   const int rot =
       nfull > 1 ? (int)(((uint64_t)((uint32_t)r * 2654435769u) * (uint32_t)nfull) >> 32) : 0;
