@@ -217,6 +217,19 @@ int prepare_partial(const kf_shape* shape, const void* q, const void* k_pool, co
   a.num_units_routes = num_launch;
   a.chunk_pages = plan.chunk_pages;
   a.max_chunks = plan.max_chunks;
+  // unsplit bf16 launches over the whole table with at least two units per
+  // CU, none longer than kMaxPagesTwoUnit pages: two units per 512-thread
+  // workgroup, one workgroup per CU, so the two units a CU holds progress
+  // evenly (units of 16384 pages ran 1.1% slower this way).  Launches over
+  // a route list keep one unit per workgroup: they are made to run beside
+  // another launch, and a 512-thread workgroup can only start on a CU that
+  // the other launch has left entirely (the agentic query-first step took
+  // 1402 us this way against 1257 us).
+  a.units_per_wg = (!fp8 && !route_list && plan.max_chunks == 1 &&
+                    max_pages_per_route <= kf::kMaxPagesTwoUnit &&
+                    (int64_t)num_launch * shape->num_kv_heads >= 2 * (int64_t)kf::cu_count())
+                       ? 2
+                       : 1;
   a.num_pages = shape->num_pages;
   a.num_page_ids = shape->num_page_ids;
   a.scale_log2 = (float)((double)shape->scale * 1.4426950408889634074);

@@ -14,8 +14,9 @@ namespace kf {
 // sizing on the host.
 constexpr int kPage = KF_PAGE_SIZE;   // tokens per page
 constexpr int kDim = KF_HEAD_DIM;     // head dimension
-constexpr int kWaves = 4;             // waves per workgroup
+constexpr int kWaves = 4;             // waves per unit (a workgroup, or half of one)
 constexpr int kMinSplitPages = 16;    // smallest page range a split workgroup gets
+constexpr int kMaxPagesTwoUnit = 2048;  // longest units run two per workgroup (bf16, unsplit)
 
 struct AppendArgs {
   void* k_pool;
@@ -49,6 +50,7 @@ struct PartialArgs {
   int32_t num_routes, max_pages_per_route;
   int32_t num_units_routes;  // routes launched: num_list, or num_routes without a list
   int32_t chunk_pages, max_chunks;  // a unit of n pages uses ceil(n / chunk_pages) workgroups
+  int32_t units_per_wg;  // 2: unsplit bf16 launch, two units per 512-thread workgroup
   int32_t num_pages, num_page_ids;
   float scale_log2;     // scale * log2(e): scores are kept in the base-2 domain
   // Fused tail append (kf_decode_step; all NULL otherwise): the route that is

@@ -5,9 +5,10 @@
 //   merge_kernel    -- log-sum-exp merge of the partials of each sequence
 //
 // partial_kernel is HBM-bound (4 flop per KV byte at 4 query heads per KV
-// head).  One 256-thread workgroup (four waves, two workgroups per CU) owns a
-// (route, KV head) unit -- or, when the host plans chunks, one of its
-// ceil(pages / chunk_pages) page ranges.  Wave w takes tiles w, w+4, ... of
+// head).  Four waves own a (route, KV head) unit -- or, when the host plans
+// chunks, one of its ceil(pages / chunk_pages) page ranges: a 256-thread
+// workgroup, two per CU, or one half of a 512-thread workgroup that holds
+// two short unsplit bf16 units, one per CU.  Wave w takes tiles w, w+4, ... of
 // the range, its full tiles taken from a per-route starting offset, so the
 // summation order is fixed and results are bitwise reproducible (and the
 // same for any placement of the pages).  Each wave streams tiles of 2 (bf16)
@@ -262,15 +263,15 @@ __device__ __forceinline__ RouteView read_route(const PartialArgs& a, int r) {
   return v;
 }
 
-// Fused step: write the step's token of KV head g into the route's page,
-// then make it visible to every wave of this workgroup before any of them
-// loads the page (waves of a workgroup share the compute unit's L1).  fp8
-// pools follow the E4M3 append rule (waves 0 and 1 take K and V) and hand
-// the page's new scales to the workgroup in s_app[0..1]: the scalar cache is
-// not coherent with vector stores, so the tail page's scales must not be
-// read back through scalar loads in this launch.
+// Fused step: write the step's token of KV head g into the route's page
+// (publish_to_workgroup then makes it visible to every wave of the
+// workgroup before any of them loads the page).  fp8 pools follow the E4M3
+// append rule (waves 0 and 1 take K and V) and hand the page's new scales to
+// the workgroup in s_app[0..1]: the scalar cache is not coherent with vector
+// stores, so the tail page's scales must not be read back through scalar
+// loads in this launch.  tid: thread index within the unit's 256 threads.
 template <bool FP8>
-__device__ __forceinline__ void write_new_token(const PartialArgs& a, const RouteView& rv, int g,
+__device__ __forceinline__ void store_new_token(const PartialArgs& a, const RouteView& rv, int g,
                                                 int tid, float* s_app) {
   const int H = a.num_kv_heads;
   const uint16_t* kn = a.k_new + ((size_t)rv.seq * H + g) * kDim;
@@ -294,6 +295,11 @@ __device__ __forceinline__ void write_new_token(const PartialArgs& a, const Rout
       }
     }
   }
+}
+
+// Orders the workgroup's earlier global stores before every later load of
+// its waves (the waves of a workgroup share the compute unit's L1).
+__device__ __forceinline__ void publish_to_workgroup() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
   __syncthreads();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
@@ -345,19 +351,39 @@ __device__ __forceinline__ T pick4(T v0, T v1, T v2, T v3, int i) {
   return (i & 2) ? ((i & 1) ? v3 : v2) : ((i & 1) ? v1 : v0);
 }
 
-template <bool FP8>
-__global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
+// UPW = units per workgroup.  1: a 256-thread workgroup owns one (route, KV
+// head) unit or one chunk of it, two workgroups per CU.  2 (unsplit bf16
+// launches of units of at most kMaxPagesTwoUnit pages): a 512-thread
+// workgroup owns units u and u + gridDim.z, waves 0-3 the first and 4-7 the
+// second, one workgroup per CU.  Of two workgroups sharing a CU the one
+// dispatched first streams faster and finishes about a third earlier, and the
+// CU then streams with four waves at lower bandwidth; the two halves of one
+// workgroup progress evenly.  In that mode all 512 threads reach every
+// barrier: a half without work (no unit, a bad or empty one) skips its
+// work, never the barriers.
+template <bool FP8, int UPW>
+__global__ __launch_bounds__(kThreads * UPW, 2 / UPW) void partial_kernel(PartialArgs a) {
   using GeoT = Geo<FP8>;
   constexpr int TP = GeoT::TP, NC = GeoT::NC, NH = GeoT::NH;
-  __shared__ float s_o[kWaves][KF_MAX_GROUP][kLdsStride];
-  __shared__ float s_m[kWaves][KF_MAX_GROUP];
-  __shared__ float s_l[kWaves][KF_MAX_GROUP];
-  __shared__ float s_fm[KF_MAX_GROUP];
-  __shared__ float s_fl[KF_MAX_GROUP];
-  __shared__ float s_app[2];  // fused fp8 append: the tail page's new K and V scales
+  __shared__ float s_o_u[UPW][kWaves][KF_MAX_GROUP][kLdsStride];
+  __shared__ float s_m_u[UPW][kWaves][KF_MAX_GROUP];
+  __shared__ float s_l_u[UPW][kWaves][KF_MAX_GROUP];
+  __shared__ float s_fm_u[UPW][KF_MAX_GROUP];
+  __shared__ float s_fl_u[UPW][KF_MAX_GROUP];
+  __shared__ float s_app_u[UPW][2];  // fused fp8 append: the tail page's new K and V scales
+  // Each wave's half is uniform, but taking it into a scalar register
+  // (readfirstlane) made the compiler keep the main loop's next tile in
+  // flight for less of each iteration: 2% slower on the Llama layer.
+  const int half = UPW == 2 ? (int)(threadIdx.x / kThreads) : 0;
+  auto& s_o = s_o_u[half];
+  auto& s_m = s_m_u[half];
+  auto& s_l = s_l_u[half];
+  auto& s_fm = s_fm_u[half];
+  auto& s_fl = s_fl_u[half];
+  float* s_app = s_app_u[half];
 
   const int c = blockIdx.x;
-  int g = blockIdx.y, u = blockIdx.z;  // u: position in the launch
+  int g = blockIdx.y, u = blockIdx.z + half * gridDim.z;  // u: position in the launch
   if constexpr (FP8) {
     // Unsplit fp8 units: workgroups are dealt round-robin over the 8 XCDs.
     // Give XCD k the k-th eighth of the (head, route) space instead, so the
@@ -372,35 +398,50 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
     }
   }
   const int G = a.group, Hq = a.num_q_heads, H = a.num_kv_heads;
-  const int tid = threadIdx.x, lane = tid & 63, grp = lane >> 4, li = lane & 15;
+  const int tid = threadIdx.x & (kThreads - 1), lane = tid & 63, grp = lane >> 4, li = lane & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int hq0 = g * G;
 
-  const int r = a.route_list ? a.route_list[u] : u;
-  if (r < 0 || r >= a.num_routes) {  // a list entry naming no route: nothing to write
-    if (c == 0 && g == 0 && tid == 0) atomicOr(a.err_flags, KF_EFLAG_BAD_ROUTE);
-    return;
-  }
-  const RouteView rv = read_route(a, r);
-  if (rv.bad || rv.npages == 0) {
-    if (c == 0) {
-      if (rv.app) write_new_token<FP8>(a, rv, g, tid, s_app);  // the pool takes the token all the same
-      const float ov = rv.bad ? qnan() : 0.0f, lv = rv.bad ? qnan() : neg_inf();
-      for (int e = tid; e < G * kDim; e += kThreads)
-        a.o_part[((size_t)r * Hq + hq0 + e / kDim) * kDim + e % kDim] = ov;
-      if (tid < G) a.lse_part[(size_t)r * Hq + hq0 + tid] = lv;
-      if (rv.bad && tid == 0) atomicOr(a.err_flags, KF_EFLAG_BAD_ROUTE);
+  // ---- this unit's page range [p0, p1), or no work for this half: outputs
+  // of a bad or empty route are written here
+  bool work = false, writer = false;
+  int r = -1, nchunks = 1, p0 = 0, p1 = 0;
+  RouteView rv{};
+  if (u < a.num_units_routes) {
+    r = a.route_list ? a.route_list[u] : u;
+    if (r < 0 || r >= a.num_routes) {  // a list entry naming no route: nothing to write
+      if (c == 0 && g == 0 && tid == 0) atomicOr(a.err_flags, KF_EFLAG_BAD_ROUTE);
+    } else {
+      rv = read_route(a, r);
+      if (rv.bad || rv.npages == 0) {
+        if (c == 0) {
+          if (rv.app) store_new_token<FP8>(a, rv, g, tid, s_app);  // the pool takes the token all the same
+          const float ov = rv.bad ? qnan() : 0.0f, lv = rv.bad ? qnan() : neg_inf();
+          for (int e = tid; e < G * kDim; e += kThreads)
+            a.o_part[((size_t)r * Hq + hq0 + e / kDim) * kDim + e % kDim] = ov;
+          if (tid < G) a.lse_part[(size_t)r * Hq + hq0 + tid] = lv;
+          if (rv.bad && tid == 0) atomicOr(a.err_flags, KF_EFLAG_BAD_ROUTE);
+        }
+      } else {
+        nchunks = (rv.npages + a.chunk_pages - 1) / a.chunk_pages;
+        if (c < nchunks) {
+          work = true;
+          writer = rv.app && c == nchunks - 1;  // the chunk with the last page
+          p0 = (int)((int64_t)c * rv.npages / nchunks);
+          p1 = (int)((int64_t)(c + 1) * rv.npages / nchunks);
+        }
+      }
     }
-    return;
   }
-  const int seq = rv.seq, n = rv.n, npages = rv.npages;
-  const int nchunks = (npages + a.chunk_pages - 1) / a.chunk_pages;
-  if (c >= nchunks) return;
-  const bool writer = rv.app && c == nchunks - 1;  // the chunk with the last page
-  if (writer) write_new_token<FP8>(a, rv, g, tid, s_app);
+  if (writer) store_new_token<FP8>(a, rv, g, tid, s_app);
+  if constexpr (UPW == 1) {
+    if (!work) return;
+    if (writer) publish_to_workgroup();
+  } else {
+    publish_to_workgroup();
+  }
+  const int seq = rv.seq, n = rv.n;
   const int app_page = (rv.n - 1) >> 4;             // route-local page of the new token
-  const int p0 = (int)((int64_t)c * npages / nchunks);
-  const int p1 = (int)((int64_t)(c + 1) * npages / nchunks);
   const int ntiles = (p1 - p0 + TP - 1) / TP;
   const int lim = min(n, p1 * kPage);  // route-local token bound of this range
   const int32_t* __restrict__ pids = a.page_ids + rv.base;
@@ -499,7 +540,8 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
 #pragma unroll
   for (int kk = 0; kk < 4; ++kk) {
     const int d0 = FP8 ? 64 * (kk >> 1) + 16 * grp + 8 * (kk & 1) : 32 * kk + 8 * grp;
-    qb[kk] = li < G ? ld16(a.q + ((size_t)seq * Hq + hq0 + li) * kDim + d0) : u32x4{0, 0, 0, 0};
+    qb[kk] = work && li < G ? ld16(a.q + ((size_t)seq * Hq + hq0 + li) * kDim + d0)
+                           : u32x4{0, 0, 0, 0};
   }
 
   f32x4 oacc[8];
@@ -673,6 +715,7 @@ __global__ __launch_bounds__(kThreads, 2) void partial_kernel(PartialArgs a) {
   }
   if (tid == 0 && wave_bad) atomicOr(a.err_flags, KF_EFLAG_BAD_PAGE);
   __syncthreads();
+  if (!work) return;  // after the workgroup's last barrier
 
   if (nchunks == 1) {
     for (int e = tid; e < G * kDim; e += kThreads) {
@@ -853,11 +896,17 @@ hipError_t launch_append(const AppendArgs& a, bool fp8, hipStream_t stream) {
 
 hipError_t launch_partial(const PartialArgs& a, bool fp8, hipStream_t stream) {
   if (a.num_units_routes == 0) return hipSuccess;
+  if (!fp8 && a.units_per_wg == 2) {
+    const dim3 grid(1, a.num_kv_heads, (a.num_units_routes + 1) / 2);
+    hipLaunchKernelGGL(HIP_KERNEL_NAME(partial_kernel<false, 2>), grid, dim3(2 * kThreads), 0,
+                       stream, a);
+    return hipGetLastError();
+  }
   const dim3 grid(a.max_chunks, a.num_kv_heads, a.num_units_routes);
   if (fp8)
-    hipLaunchKernelGGL(partial_kernel<true>, grid, dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL(HIP_KERNEL_NAME(partial_kernel<true, 1>), grid, dim3(kThreads), 0, stream, a);
   else
-    hipLaunchKernelGGL(partial_kernel<false>, grid, dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL(HIP_KERNEL_NAME(partial_kernel<false, 1>), grid, dim3(kThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.max_chunks == 1) return e;
   hipLaunchKernelGGL(combine_kernel, dim3(a.num_kv_heads, a.num_units_routes), dim3(kThreads), 0,
