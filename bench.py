@@ -201,6 +201,18 @@ def policy_report(inst, wl, bw_gbps: float, attn_us: float, hbm_bytes: int) -> d
                            "T_step = layers x measured attention+merge, T_prewarm 1 s"}
 
 
+def kernel_label(st, wl) -> str:
+    """The partial-attention launch the timed step makes, from the library's
+    own plan: its kernel, units per workgroup and any combine launch."""
+    from paper_2606_29207_amd import kf
+    chunk_pages, max_chunks, units = kf.partial_attn_plan(st.shape, st.routes.shape[0],
+                                                          st.max_pages_per_route)
+    name = f"partial_kernel<{wl.kv_dtype}" + (", 2 units/workgroup>" if units == 2 else ">")
+    if max_chunks > 1:
+        name += f" + combine_kernel ({chunk_pages}-page chunks, up to {max_chunks} per unit)"
+    return name
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -386,8 +398,7 @@ def main(argv=None):
         "attn_merge_us": round(float((t_par + t_mrg).mean()), 2),
         "attn_merge_GBps": round(am_b / ((t_par + t_mrg).mean() * 1e-6) / 1e9, 2),
         "bytes_per_step": int(step_b),
-        "roofline": {"bound": "hbm", "kernel": "partial_kernel<bf16>" if wl.kv_dtype == "bf16"
-                     else "partial_kernel<fp8>",
+        "roofline": {"bound": "hbm", "kernel": kernel_label(st, wl),
                      "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic, "algorithmic_bytes_per_launch": int(par_b)},

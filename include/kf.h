@@ -140,6 +140,27 @@ size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes
                                        int32_t max_pages_per_route);
 
 /*
+ * kf_partial_attn_plan -- how a partial-attention launch of `num_launch`
+ * routes of at most `max_pages_per_route` pages runs on the current device:
+ * kf_partial_attn and kf_decode_step (route_list_launch = 0), or
+ * kf_partial_attn_subset over a list of num_launch routes
+ * (route_list_launch = 1).  Not an operation of the paper: a description of
+ * this implementation's launch, for callers that size or inspect it.
+ *   *chunk_pages  pages per workgroup range; a unit of n pages is cut into
+ *                 ceil(n / chunk_pages) ranges
+ *   *max_chunks   most ranges per unit; 1 = every unit whole, no combine
+ *                 launch and no workspace use
+ *   *units_per_wg 1 or 2 (route, KV head) units per workgroup
+ * Host only; launches nothing.  Any output pointer may be NULL.  Returns
+ * KF_OK, KF_ERR_INVALID_ARG (null or invalid shape, negative sizes,
+ * route_list_launch not 0 or 1) or KF_ERR_UNSUPPORTED (a shape or size the
+ * kernels do not take, as kf_partial_attn would report).
+ */
+int kf_partial_attn_plan(const kf_shape* shape, int32_t num_launch, int32_t max_pages_per_route,
+                         int32_t route_list_launch, int32_t* chunk_pages, int32_t* max_chunks,
+                         int32_t* units_per_wg);
+
+/*
  * kf_partial_attn -- local core attention of every route (Section 3.2,
  * step 3): for route r of sequence b and query head h,
  *   s_t = scale * (q[b][h] . k_t) over the route's resident tokens t,

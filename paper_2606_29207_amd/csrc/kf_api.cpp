@@ -78,6 +78,24 @@ ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_page
   return {(int32_t)c, (int32_t)m};
 }
 
+// Unsplit bf16 launches over the whole table with at least two units per
+// CU, none longer than kMaxPagesTwoUnit pages, run two units per 512-thread
+// workgroup, one workgroup per CU.  Both units of a CU then start at once:
+// with 256-thread workgroups the second workgroup of each CU started ~3 us
+// after the first, and the Llama layer ran 1.2-1.4% slower.  Units of 16384
+// pages ran 1.1% slower in this mode.  Launches over a route list keep one
+// unit per workgroup: they are made to run beside another launch, and a
+// 512-thread workgroup needs the registers of a whole CU, so it waits until
+// the other launch has left one entirely (the agentic query-first step took
+// 1402 us this way against 1257 us).
+int32_t units_per_workgroup(bool fp8, bool route_list, const ChunkPlan& plan, int32_t num_launch,
+                            int32_t num_kv_heads, int32_t max_pages_per_route) {
+  return !fp8 && !route_list && plan.max_chunks == 1 && max_pages_per_route <= kMaxPagesTwoUnit &&
+                 (int64_t)num_launch * num_kv_heads >= 2 * (int64_t)cu_count()
+             ? 2
+             : 1;
+}
+
 WorkspaceLayout workspace_layout(int32_t num_routes, int32_t num_kv_heads, int32_t group,
                                  int32_t max_chunks) {
   WorkspaceLayout l;
@@ -123,6 +141,24 @@ size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes
     if (t > most) most = t;
   }
   return most;
+}
+
+int kf_partial_attn_plan(const kf_shape* shape, int32_t num_launch, int32_t max_pages_per_route,
+                         int32_t route_list_launch, int32_t* chunk_pages, int32_t* max_chunks,
+                         int32_t* units_per_wg) {
+  const int st = check_shape(shape);
+  if (st != KF_OK) return st;
+  if (num_launch < 0 || max_pages_per_route < 0 || (route_list_launch != 0 && route_list_launch != 1))
+    return KF_ERR_INVALID_ARG;
+  if (num_launch > 65535 || shape->num_kv_heads > 65535) return KF_ERR_UNSUPPORTED;
+  const kf::ChunkPlan plan = kf::plan_chunks(num_launch, shape->num_kv_heads, max_pages_per_route);
+  if (chunk_pages) *chunk_pages = plan.chunk_pages;
+  if (max_chunks) *max_chunks = plan.max_chunks;
+  if (units_per_wg)
+    *units_per_wg = kf::units_per_workgroup(shape->kv_dtype == KF_KV_FP8_E4M3,
+                                            route_list_launch == 1, plan, num_launch,
+                                            shape->num_kv_heads, max_pages_per_route);
+  return KF_OK;
 }
 
 }  // extern "C"
@@ -217,19 +253,8 @@ int prepare_partial(const kf_shape* shape, const void* q, const void* k_pool, co
   a.num_units_routes = num_launch;
   a.chunk_pages = plan.chunk_pages;
   a.max_chunks = plan.max_chunks;
-  // unsplit bf16 launches over the whole table with at least two units per
-  // CU, none longer than kMaxPagesTwoUnit pages: two units per 512-thread
-  // workgroup, one workgroup per CU, so the two units a CU holds progress
-  // evenly (units of 16384 pages ran 1.1% slower this way).  Launches over
-  // a route list keep one unit per workgroup: they are made to run beside
-  // another launch, and a 512-thread workgroup can only start on a CU that
-  // the other launch has left entirely (the agentic query-first step took
-  // 1402 us this way against 1257 us).
-  a.units_per_wg = (!fp8 && !route_list && plan.max_chunks == 1 &&
-                    max_pages_per_route <= kf::kMaxPagesTwoUnit &&
-                    (int64_t)num_launch * shape->num_kv_heads >= 2 * (int64_t)kf::cu_count())
-                       ? 2
-                       : 1;
+  a.units_per_wg = kf::units_per_workgroup(fp8, route_list != nullptr, plan, num_launch,
+                                           shape->num_kv_heads, max_pages_per_route);
   a.num_pages = shape->num_pages;
   a.num_page_ids = shape->num_page_ids;
   a.scale_log2 = (float)((double)shape->scale * 1.4426950408889634074);

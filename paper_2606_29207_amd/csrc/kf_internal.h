@@ -95,6 +95,10 @@ struct ChunkPlan {
   int32_t chunk_pages, max_chunks;
 };
 ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_pages_per_route);
+// Units per workgroup of a partial-attention launch of num_launch routes
+// (1 or 2); route_list: a launch over a route list (kf_partial_attn_subset).
+int32_t units_per_workgroup(bool fp8, bool route_list, const ChunkPlan& plan, int32_t num_launch,
+                            int32_t num_kv_heads, int32_t max_pages_per_route);
 WorkspaceLayout workspace_layout(int32_t num_routes, int32_t num_kv_heads, int32_t group,
                                  int32_t max_chunks);
 

@@ -355,12 +355,9 @@ __device__ __forceinline__ T pick4(T v0, T v1, T v2, T v3, int i) {
 // head) unit or one chunk of it, two workgroups per CU.  2 (unsplit bf16
 // launches of units of at most kMaxPagesTwoUnit pages): a 512-thread
 // workgroup owns units u and u + gridDim.z, waves 0-3 the first and 4-7 the
-// second, one workgroup per CU.  Of two workgroups sharing a CU the one
-// dispatched first streams faster and finishes about a third earlier, and the
-// CU then streams with four waves at lower bandwidth; the two halves of one
-// workgroup progress evenly.  In that mode all 512 threads reach every
-// barrier: a half without work (no unit, a bad or empty one) skips its
-// work, never the barriers.
+// second, one workgroup per CU, so both units of a CU start at once.  In
+// that mode all 512 threads reach every barrier: a half without work (no
+// unit, a bad or empty one) skips its work, never the barriers.
 template <bool FP8, int UPW>
 __global__ __launch_bounds__(kThreads * UPW, 2 / UPW) void partial_kernel(PartialArgs a) {
   using GeoT = Geo<FP8>;

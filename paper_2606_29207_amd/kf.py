@@ -33,9 +33,9 @@ EFLAG_BAD_ROUTE = 2
 EFLAG_BAD_PAGE = 4
 
 # every symbol include/kf.h declares
-EXPORTS = ("kf_kv_append", "kf_partial_attn_workspace_bytes", "kf_partial_attn",
-           "kf_partial_attn_subset", "kf_merge_partials", "kf_decode_step", "kf_debug_gather",
-           "kf_status_str", "kf_version")
+EXPORTS = ("kf_kv_append", "kf_partial_attn_workspace_bytes", "kf_partial_attn_plan",
+           "kf_partial_attn", "kf_partial_attn_subset", "kf_merge_partials", "kf_decode_step",
+           "kf_debug_gather", "kf_status_str", "kf_version")
 
 
 class KFError(RuntimeError):
@@ -73,6 +73,8 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.kf_kv_append.restype = ctypes.c_int
     lib.kf_partial_attn_workspace_bytes.argtypes = [sp, i32, i32]
     lib.kf_partial_attn_workspace_bytes.restype = sz
+    lib.kf_partial_attn_plan.argtypes = [sp, i32, i32, i32, vp, vp, vp]
+    lib.kf_partial_attn_plan.restype = ctypes.c_int
     lib.kf_partial_attn.argtypes = [sp, vp, vp, vp, vp, vp, vp, i32, i32, vp, vp, vp, vp, sz, vp, vp]
     lib.kf_partial_attn.restype = ctypes.c_int
     lib.kf_partial_attn_subset.argtypes = [sp, vp, vp, vp, vp, vp, vp, i32, vp, i32, i32, vp, vp, vp,
@@ -190,6 +192,17 @@ def kv_append(shape: Shape, k_pool, v_pool, k_new, v_new, routes, tail_route, pa
 def partial_attn_workspace_bytes(shape: Shape, num_routes: int, max_pages_per_route: int) -> int:
     return int(load().kf_partial_attn_workspace_bytes(ctypes.byref(shape), num_routes,
                                                        max_pages_per_route))
+
+
+def partial_attn_plan(shape: Shape, num_launch: int, max_pages_per_route: int,
+                      route_list: bool = False) -> tuple[int, int, int]:
+    """kf_partial_attn_plan: (chunk_pages, max_chunks, units_per_wg) of a
+    launch of num_launch routes (route_list: a kf_partial_attn_subset launch)."""
+    out = [ctypes.c_int32(0) for _ in range(3)]
+    st = load().kf_partial_attn_plan(ctypes.byref(shape), int(num_launch), int(max_pages_per_route),
+                                     1 if route_list else 0, *[ctypes.byref(o) for o in out])
+    _check(st, "kf_partial_attn_plan")
+    return tuple(int(o.value) for o in out)
 
 
 def alloc_workspace(shape: Shape, num_routes: int, max_pages_per_route: int, device="cuda"):

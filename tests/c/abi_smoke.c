@@ -1,6 +1,7 @@
 /* Plain C99 client of libkf: the headers compile as C, and the host entry
- * points (status strings, version, the scaling-policy calculator of
- * Section 4.2 on the hand-worked example) run without a GPU. */
+ * points (status strings, version, the launch-plan query, the
+ * scaling-policy calculator of Section 4.2 on the hand-worked example) run
+ * without a GPU. */
 #include <math.h>
 #include <stdio.h>
 #include <string.h>
@@ -43,6 +44,14 @@ int main(void) {
   if (strncmp(kf_version(), "kf ", 3) != 0) fails |= 128;
   if (sizeof(kf_route) != 24 || sizeof(kf_policy_params) != 80 || sizeof(kf_policy_node) != 32)
     fails |= 256;
+
+  /* launch plan of the Llama-3.1-8B layer (no GPU: 256 compute units assumed) */
+  const kf_shape llama = {16, 32, 8, KF_HEAD_DIM, KF_PAGE_SIZE, KF_KV_BF16, 33000, 33000, 0.0884f};
+  int32_t chunk_pages = 0, max_chunks = 0, units_per_wg = 0;
+  if (kf_partial_attn_plan(&llama, 64, 516, 0, &chunk_pages, &max_chunks, &units_per_wg) != KF_OK ||
+      chunk_pages != 516 || max_chunks != 1 || units_per_wg != 2)
+    fails |= 512;
+  if (kf_partial_attn_plan(&llama, 64, 516, 2, NULL, NULL, NULL) != KF_ERR_INVALID_ARG) fails |= 1024;
   printf("abi_smoke %s (%d)\n", fails ? "FAILED" : "ok", fails);
   return fails ? 1 : 0;
 }

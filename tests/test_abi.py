@@ -216,6 +216,41 @@ def test_workspace_bytes(lib):
     assert kf.partial_attn_workspace_bytes(_shape(head_dim=64), 4, 5) == 0
 
 
+def test_partial_attn_plan(lib):
+    """Launch plans without a GPU (256 compute units assumed: 512 resident
+    workgroups).  Whole-table bf16 launches of at least 512 unsplit units of
+    at most 2048 pages run two units per workgroup; fp8, route-list and
+    chunked launches one."""
+    s = _shape(num_seqs=16, num_q_heads=32, num_kv_heads=8, num_pages=40000, num_page_ids=40000)
+    plan = kf.partial_attn_plan
+    assert plan(s, 64, 516) == (516, 1, 2)                  # Llama layer: 512 units, unsplit
+    assert plan(s, 64, 516, route_list=True) == (516, 1, 1)
+    assert plan(s, 64, 2048) == (2048, 1, 2)
+    assert plan(s, 64, 2049) == (2049, 1, 1)                # longer units: one per workgroup
+    assert plan(s, 128, 1024) == (1024, 1, 2)               # two rounds of units
+    c, m, u = plan(s, 63, 516)                              # 504 units: split, combine launch
+    assert m > 1 and u == 1 and c * m >= 516 and c * (m - 1) < 516
+    fp8 = _shape(num_seqs=32, num_q_heads=64, num_kv_heads=8, kv_dtype=kf.KV_FP8_E4M3,
+                 num_pages=10, num_page_ids=10)
+    assert plan(fp8, 128, 1024) == (1024, 1, 1)
+    tiny = _shape(num_seqs=1, num_q_heads=8, num_kv_heads=2, num_pages=256, num_page_ids=256)
+    assert plan(tiny, 2, 128) == (16, 8, 1)                 # 4 units: 8 splits of 16 pages
+    assert plan(tiny, 2, 16) == (16, 1, 1)                  # too short to split
+    assert plan(tiny, 0, 16) == (16, 1, 1)
+    # errors: null outputs are allowed, bad sizes and shapes are not
+    i32 = ctypes.c_int32
+    assert lib.kf_partial_attn_plan(ctypes.byref(s), 64, 516, 0, None, None, None) == 0
+    out = [i32(-7) for _ in range(3)]
+    refs = [ctypes.byref(o) for o in out]
+    for args, status in (((-1, 5, 0), kf.ERR_INVALID_ARG), ((4, -1, 0), kf.ERR_INVALID_ARG),
+                         ((4, 5, 2), kf.ERR_INVALID_ARG), ((65536, 5, 0), kf.ERR_UNSUPPORTED)):
+        assert lib.kf_partial_attn_plan(ctypes.byref(s), *args, *refs) == status
+    assert lib.kf_partial_attn_plan(None, 4, 5, 0, *refs) == kf.ERR_INVALID_ARG
+    assert lib.kf_partial_attn_plan(ctypes.byref(_shape(head_dim=64)), 4, 5, 0,
+                                    *refs) == kf.ERR_UNSUPPORTED
+    assert [o.value for o in out] == [-7, -7, -7]           # nothing written on error
+
+
 def test_debug_gather_host_checks(lib):
     v = lambda x: None if x is None else ctypes.c_void_p(x)  # noqa: E731
     s = _shape()

@@ -1,7 +1,7 @@
 """Unsplit bf16 launches that run two (route, KV head) units per 512-thread
-workgroup (units u and u + ceil(U/2) share one).  Every shape here has at
-least 512 units of at most 16 pages, so the plan is unsplit and two units go
-to each workgroup; an odd route count leaves the last workgroup half idle.
+workgroup (units u and u + ceil(U/2) share one).  Every shape here is
+planned that way, which each test checks through kf_partial_attn_plan; an
+odd route count leaves the last workgroup half idle.
 The halves see every mix of states: a tail taking the step's token beside a
 route that does not, empty and broken routes beside working ones.  Checked
 against the oracle and, for the fused step, bit for bit against the three
@@ -32,8 +32,16 @@ def _instance(seed, steps):
     return inst
 
 
+def _assert_two_units(st, route_list=False):
+    from paper_2606_29207_amd import kf
+    plan = kf.partial_attn_plan(st.shape, st.routes.shape[0], st.max_pages_per_route, route_list)
+    assert plan[1:] == ((1, 1) if route_list else (1, 2)), plan
+
+
 def test_two_units_per_workgroup_match_oracle_and_separate_calls(gpu):
+    from paper_2606_29207_amd.step import DecodeState
     inst = _instance(seed=21, steps=3)
+    _assert_two_units(DecodeState.from_instance(inst))
     o = run_oracle(inst, 3)
     f = host(run_gpu(inst, 3, fused=True))
     compare_all(f, o)
@@ -62,6 +70,7 @@ def test_two_units_per_workgroup_with_broken_rows(gpu):
                          page_ids=page_ids, seq_route_begin=inst.seq_route_begin,
                          tail_route=tail, scale=inst.scale,
                          max_pages_per_route=inst.max_pages_per_route)
+        _assert_two_units(st)
         for s in range(2):
             kn, vn = st.upload_new_tokens(*inst.new_tokens(s))
             (st.step_fused if fused else st.step)(kn, vn)
@@ -102,6 +111,8 @@ def test_two_units_per_workgroup_bitwise_equal_to_one(gpu, shape):
         inst = make_instance(wl, seed=24, steps=1, seq_lens=[8192] * 16)
         assert len(inst.routes) * wl.num_kv_heads == 512
     st = DecodeState.from_instance(inst)
+    _assert_two_units(st)
+    _assert_two_units(st, route_list=True)
     st.partial()
     torch.cuda.synchronize()
     o2, l2 = st.o_part.clone(), st.lse_part.clone()
