@@ -1,0 +1,57 @@
+"""Seeded random shapes through the whole step, against the oracle: KV dtype,
+KV heads, group size, sequence count and lengths (empty and page-edge ones
+included), route length, pool placement, appends and step count are all
+drawn from one generator per case.  Every fourth case draws many short
+routes, so that launches with at least 512 unsplit units (two units per
+workgroup for bf16) are among them; the others mostly split their units.
+The plan each case takes is checked to be a valid one."""
+import numpy as np
+import pytest
+
+from kf_testlib import compare_all, host, run_gpu, run_oracle
+from kf_workloads import make_instance, workload
+
+pytestmark = [pytest.mark.gpu, pytest.mark.filterwarnings("ignore::RuntimeWarning")]
+
+EDGE_LENS = (0, 1, 15, 16, 17, 31, 32, 33)
+
+
+def draw(case):
+    rng = np.random.default_rng([2606, 29207, case])
+    fp8 = bool(rng.random() < 0.35)
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    group = int(rng.integers(1, 17))
+    many = case % 4 == 0
+    if many:        # many routes of at most 15 pages, tails included
+        B = int(rng.integers(20, 41))
+        part = 16 * int(rng.integers(1, 14))
+        lens = rng.integers(100, 1500, B)
+    else:
+        B = int(rng.integers(1, 13))
+        part = 16 * int(rng.integers(1, 160))
+        lens = rng.integers(0, 4000, B)
+    for i in range(B):
+        if rng.random() < 0.2:
+            lens[i] = EDGE_LENS[int(rng.integers(len(EDGE_LENS)))]
+    appends = int(rng.random() < 0.7)
+    steps = int(rng.integers(1, 4)) if appends else 1
+    over = dict(num_seqs=B, num_q_heads=group * hkv, num_kv_heads=hkv, part_tokens=part,
+                appends=appends, permuted=bool(rng.random() < 0.5))
+    wl = workload("wide_gqa_fp8" if fp8 else "llama8b_32k", **over)
+    return make_instance(wl, seed=1000 + case, steps=steps, seq_lens=[int(x) for x in lens]), steps
+
+
+@pytest.mark.parametrize("case", range(48))
+def test_random_shape(gpu, case):
+    from paper_2606_29207_amd import kf
+    from paper_2606_29207_amd.step import DecodeState
+    inst, steps = draw(case)
+    st = DecodeState.from_instance(inst)
+    chunk_pages, max_chunks, units = kf.partial_attn_plan(st.shape, st.routes.shape[0],
+                                                          st.max_pages_per_route)
+    assert chunk_pages * max_chunks >= inst.max_pages_per_route and units in (1, 2)
+    assert units == 1 or (inst.wl.kv_dtype == "bf16" and max_chunks == 1)
+    del st
+    o = run_oracle(inst, steps)
+    g = host(run_gpu(inst, steps, fused=bool(inst.wl.appends)))
+    compare_all(g, o)
