@@ -742,10 +742,14 @@ __global__ __launch_bounds__(kThreads * UPW, 2 / UPW) void partial_kernel(Partia
 }
 
 // Combine the chunk partials of each chunked (route, KV head) in chunk order.
+// Wave w reduces heads w, w+4, ...: its lanes read up to 64 chunks' (max,
+// sum) at once; then every thread sums its output elements over the chunks
+// in chunk order, four chunks' loads in flight at a time.
 __global__ __launch_bounds__(kThreads) void combine_kernel(PartialArgs a) {
   __shared__ float s_fm[KF_MAX_GROUP];
   __shared__ float s_fl[KF_MAX_GROUP];
   const int g = blockIdx.x, u = blockIdx.y, tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6;
   const int G = a.group, Hq = a.num_q_heads, H = a.num_kv_heads;
   const int r = a.route_list ? a.route_list[u] : u;
   if (r < 0 || r >= a.num_routes) return;  // flagged by partial_kernel
@@ -754,16 +758,21 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(PartialArgs a) {
   const int nchunks = (rv.npages + a.chunk_pages - 1) / a.chunk_pages;
   if (nchunks == 1) return;              // written by partial_kernel
   const size_t rec0 = ((size_t)u * H + g) * a.max_chunks;
-  if (tid < G) {
+  for (int h = w; h < G; h += kWaves) {
     float M = neg_inf();
-    for (int c = 0; c < nchunks; ++c) M = fmaxf(M, a.ws_ml[((rec0 + c) * G + tid) * 2]);
+    for (int c = lane; c < nchunks; c += 64) M = fmaxf(M, a.ws_ml[((rec0 + c) * G + h) * 2]);
+    for (int m = 32; m >= 1; m >>= 1) M = fmaxf(M, __shfl_xor(M, m));
     float L = 0.0f;
-    for (int c = 0; c < nchunks; ++c) {
-      const float mc = a.ws_ml[((rec0 + c) * G + tid) * 2];
-      if (mc != neg_inf()) L += exp2_fast(mc - M) * a.ws_ml[((rec0 + c) * G + tid) * 2 + 1];
+    for (int c = lane; c < nchunks; c += 64) {
+      const float mc = a.ws_ml[((rec0 + c) * G + h) * 2];
+      const float lc = a.ws_ml[((rec0 + c) * G + h) * 2 + 1];
+      L += mc == neg_inf() ? 0.0f : exp2_fast(mc - M) * lc;
     }
-    s_fm[tid] = M;
-    s_fl[tid] = L;
+    for (int m = 32; m >= 1; m >>= 1) L += __shfl_xor(L, m);
+    if (lane == 0) {
+      s_fm[h] = M;
+      s_fl[h] = L;
+    }
   }
   __syncthreads();
   const int hq0 = g * G;
@@ -771,9 +780,11 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(PartialArgs a) {
     const int h = e / kDim, d = e % kDim;
     const float M = s_fm[h];
     float O = 0.0f;
+#pragma unroll 4
     for (int c = 0; c < nchunks; ++c) {
       const float mc = a.ws_ml[((rec0 + c) * G + h) * 2];
-      if (mc != neg_inf()) O += exp2_fast(mc - M) * a.ws_o[((rec0 + c) * G + h) * kDim + d];
+      const float oc = a.ws_o[((rec0 + c) * G + h) * kDim + d];
+      O += mc == neg_inf() ? 0.0f : exp2_fast(mc - M) * oc;
     }
     a.o_part[((size_t)r * Hq + hq0 + h) * kDim + d] = O / s_fl[h];
   }
@@ -855,26 +866,38 @@ __global__ __launch_bounds__(64) void merge_kernel(MergeArgs a) {
     return;
   }
   constexpr float kLog2e = 1.44269504088896340736f;
+  // lane i reads the lse of routes r0 + i, r0 + i + 64, ...
+  const int n = r1 - r0;
   float M = neg_inf();
-  bool any_nan = false;
-  for (int r = r0; r < r1; ++r) {
-    const float l = a.lse_part[(size_t)r * Hq + h];
-    any_nan |= l != l;
+  bool nan_seen = false;
+  for (int i = lane; i < n; i += 64) {
+    const float l = a.lse_part[(size_t)(r0 + i) * Hq + h];
+    nan_seen |= l != l;
     M = fmaxf(M, l);
   }
+  for (int m = 32; m >= 1; m >>= 1) M = fmaxf(M, __shfl_xor(M, m));
+  const bool any_nan = __ballot(nan_seen) != 0;
   if (any_nan || M == neg_inf()) {
     const float v = any_nan ? qnan() : 0.0f;
     *out = make_float2(v, v);
     if (lane == 0) *lse_out = any_nan ? qnan() : neg_inf();
     return;
   }
+  // routes in order; route base + j's weight comes from lane j
   float L = 0.0f, o0 = 0.0f, o1 = 0.0f;
-  for (int r = r0; r < r1; ++r) {
-    const float wr = exp2_fast((a.lse_part[(size_t)r * Hq + h] - M) * kLog2e);
-    const float2 v = reinterpret_cast<const float2*>(a.o_part + ((size_t)r * Hq + h) * kDim)[lane];
-    L += wr;
-    o0 += wr * v.x;
-    o1 += wr * v.y;
+  for (int base = 0; base < n; base += 64) {
+    const int i = base + lane;
+    const float wl = i < n ? exp2_fast((a.lse_part[(size_t)(r0 + i) * Hq + h] - M) * kLog2e) : 0.0f;
+    const int cnt = min(64, n - base);
+#pragma unroll 4
+    for (int j = 0; j < cnt; ++j) {
+      const float wr = __shfl(wl, j);
+      const float2 v =
+          reinterpret_cast<const float2*>(a.o_part + ((size_t)(r0 + base + j) * Hq + h) * kDim)[lane];
+      L += wr;
+      o0 += wr * v.x;
+      o1 += wr * v.y;
+    }
   }
   *out = make_float2(o0 / L, o1 / L);
   if (lane == 0) *lse_out = M + __logf(L);
