@@ -66,11 +66,21 @@ ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_page
   const int32_t whole = max_pages_per_route > 0 ? max_pages_per_route : 1;
   if (units <= 0 || max_pages_per_route <= kMinSplitPages) return {whole, 1};
   if (units >= slots && units % slots == 0) return {whole, 1};
-  const int64_t target = units < slots ? slots : 32 * slots;
+  const int64_t target = units < slots ? slots : 12 * slots;
   int64_t c = (units * max_pages_per_route + target - 1) / target;
   if (c < kMinSplitPages) c = kMinSplitPages;
   if (c >= max_pages_per_route) return {whole, 1};
   int64_t m = (max_pages_per_route + c - 1) / c;
+  // Workgroups are dealt round-robin over the 8 XCDs in launch order, chunk
+  // index fastest, so with an even chunk count the chunk index alone picks
+  // the XCD half (a multiple of 8: the XCD), and the units shorter than the
+  // longest, whose high chunk indices are empty, leave those XCDs idle.  An
+  // odd count rotates every chunk index over all XCDs.
+  if (units >= slots && m % 2 == 0) {
+    c = (max_pages_per_route + m) / (m + 1);
+    if (c < kMinSplitPages) c = kMinSplitPages;
+    m = (max_pages_per_route + c - 1) / c;
+  }
   if (m > 65535) {
     m = 65535;
     c = (max_pages_per_route + m - 1) / m;

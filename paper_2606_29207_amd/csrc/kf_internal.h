@@ -89,8 +89,9 @@ struct WorkspaceLayout {
 // How the pages of each (route, KV head) unit are spread over workgroups.
 // One workgroup owns a whole unit when the units fill whole rounds of the
 // GPU's resident workgroups (two per compute unit); otherwise units are cut
-// into chunks of chunk_pages pages, about 32 chunks per resident slot, so
-// the dispatcher balances uneven routes, and a combine kernel follows.
+// into chunks of chunk_pages pages, about 12 chunks per resident slot (an
+// odd number of chunks for the longest unit), so the dispatcher balances
+// uneven routes, and a combine kernel follows.
 struct ChunkPlan {
   int32_t chunk_pages, max_chunks;
 };

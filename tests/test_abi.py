@@ -180,17 +180,22 @@ def _workspace_need(units_routes, H, G, maxp, slots=512):
     """Bytes one launch of `units_routes` routes needs, by the planner's rule:
     units that fill whole rounds of the resident slots stay whole (no
     records); otherwise chunks of about one per slot (fewer units than
-    slots) or 32 per slot, never under 16 pages; records of (max, sum) and
-    o per query head, each array rounded up to 256 bytes."""
+    slots) or 12 per slot with an odd chunk count for the longest unit,
+    never under 16 pages; records of (max, sum) and o per query head, each
+    array rounded up to 256 bytes."""
     rup = lambda x: -(-x // 256) * 256  # noqa: E731
     units = units_routes * H
     if units == 0 or maxp <= 16 or (units >= slots and units % slots == 0):
         return 256
-    target = slots if units < slots else 32 * slots
+    target = slots if units < slots else 12 * slots
     c = max(-(-units * maxp // target), 16)
     if c >= maxp:
         return 256
-    recs = units * -(-maxp // c) * G
+    m = -(-maxp // c)
+    if units >= slots and m % 2 == 0:
+        c = max(-(-maxp // (m + 1)), 16)
+        m = -(-maxp // c)
+    recs = units * m * G
     return rup(recs * 2 * 4) + rup(recs * 128 * 4)
 
 
