@@ -60,13 +60,20 @@ int cu_count() {
 }
 }  // namespace
 
-ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_pages_per_route) {
+ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_pages_per_route,
+                      int64_t num_page_ids) {
   const int64_t units = (int64_t)num_routes * num_kv_heads;
   const int64_t slots = 2 * (int64_t)cu_count();  // resident workgroups at two per CU
   const int32_t whole = max_pages_per_route > 0 ? max_pages_per_route : 1;
   if (units <= 0 || max_pages_per_route <= kMinSplitPages) return {whole, 1};
   if (units >= slots && units % slots == 0) return {whole, 1};
-  const int64_t target = units < slots ? slots : 12 * slots;
+  // Fewer units than slots: units of equal length run best as about one
+  // range per slot, one round of workgroups.  Ragged routes need more ranges
+  // for the dispatcher to balance; they are recognised by a page table
+  // under 90% of routes x max pages (the routes' reservations sum to it).
+  const bool ragged =
+      units < slots && num_page_ids * 10 < (int64_t)num_routes * max_pages_per_route * 9;
+  const int64_t target = (units < slots ? (ragged ? 4 : 1) : 12) * slots;
   int64_t c = (units * max_pages_per_route + target - 1) / target;
   if (c < kMinSplitPages) c = kMinSplitPages;
   if (c >= max_pages_per_route) return {whole, 1};
@@ -76,7 +83,7 @@ ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_page
   // the XCD half (a multiple of 8: the XCD), and the units shorter than the
   // longest, whose high chunk indices are empty, leave those XCDs idle.  An
   // odd count rotates every chunk index over all XCDs.
-  if (units >= slots && m % 2 == 0) {
+  if ((units >= slots || ragged) && m % 2 == 0) {
     c = (max_pages_per_route + m) / (m + 1);
     if (c < kMinSplitPages) c = kMinSplitPages;
     m = (max_pages_per_route + c - 1) / c;
@@ -146,7 +153,8 @@ size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes
   // a whole route table must also serve a launch over a subset of it.
   size_t most = 0;
   for (int32_t m = num_routes > 0 ? 1 : 0; m <= num_routes; ++m) {
-    const kf::ChunkPlan plan = kf::plan_chunks(m, shape->num_kv_heads, max_pages_per_route);
+    const kf::ChunkPlan plan = kf::plan_chunks(m, shape->num_kv_heads, max_pages_per_route,
+                                               shape->num_page_ids);
     const size_t t = kf::workspace_layout(m, shape->num_kv_heads, group, plan.max_chunks).total;
     if (t > most) most = t;
   }
@@ -161,7 +169,8 @@ int kf_partial_attn_plan(const kf_shape* shape, int32_t num_launch, int32_t max_
   if (num_launch < 0 || max_pages_per_route < 0 || (route_list_launch != 0 && route_list_launch != 1))
     return KF_ERR_INVALID_ARG;
   if (num_launch > 65535 || shape->num_kv_heads > 65535) return KF_ERR_UNSUPPORTED;
-  const kf::ChunkPlan plan = kf::plan_chunks(num_launch, shape->num_kv_heads, max_pages_per_route);
+  const kf::ChunkPlan plan = kf::plan_chunks(num_launch, shape->num_kv_heads, max_pages_per_route,
+                                             shape->num_page_ids);
   if (chunk_pages) *chunk_pages = plan.chunk_pages;
   if (max_chunks) *max_chunks = plan.max_chunks;
   if (units_per_wg)
@@ -235,7 +244,8 @@ int prepare_partial(const kf_shape* shape, const void* q, const void* k_pool, co
   for (const void* p : p4)
     if (p && !aligned(p, 4)) return KF_ERR_INVALID_ARG;
   const int32_t group = shape->num_q_heads / shape->num_kv_heads;
-  const kf::ChunkPlan plan = kf::plan_chunks(num_launch, shape->num_kv_heads, max_pages_per_route);
+  const kf::ChunkPlan plan = kf::plan_chunks(num_launch, shape->num_kv_heads, max_pages_per_route,
+                                             shape->num_page_ids);
   const kf::WorkspaceLayout l =
       kf::workspace_layout(num_launch, shape->num_kv_heads, group, plan.max_chunks);
   if (!workspace || !aligned(workspace, 256) || workspace_bytes < l.total) return KF_ERR_WORKSPACE;

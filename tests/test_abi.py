@@ -176,23 +176,25 @@ def test_merge_host_checks(lib):
     assert lib.kf_merge_partials(0, 4, 8, 128, *([None] * 7), None) == 0
 
 
-def _workspace_need(units_routes, H, G, maxp, slots=512):
+def _workspace_need(units_routes, H, G, maxp, num_page_ids, slots=512):
     """Bytes one launch of `units_routes` routes needs, by the planner's rule:
     units that fill whole rounds of the resident slots stay whole (no
-    records); otherwise chunks of about one per slot (fewer units than
-    slots) or 12 per slot with an odd chunk count for the longest unit,
-    never under 16 pages; records of (max, sum) and o per query head, each
-    array rounded up to 256 bytes."""
+    records); otherwise chunks of about 12 per slot (more units than slots)
+    or about one per slot (fewer; four when the page table holds under 90%
+    of routes x max pages), never under 16 pages, an odd chunk count for the
+    longest unit except for one per slot; records of (max, sum) and o per
+    query head, each array rounded up to 256 bytes."""
     rup = lambda x: -(-x // 256) * 256  # noqa: E731
     units = units_routes * H
     if units == 0 or maxp <= 16 or (units >= slots and units % slots == 0):
         return 256
-    target = slots if units < slots else 12 * slots
+    ragged = units < slots and num_page_ids * 10 < units_routes * maxp * 9
+    target = (12 if units >= slots else 4 if ragged else 1) * slots
     c = max(-(-units * maxp // target), 16)
     if c >= maxp:
         return 256
     m = -(-maxp // c)
-    if units >= slots and m % 2 == 0:
+    if (units >= slots or ragged) and m % 2 == 0:
         c = max(-(-maxp // (m + 1)), 16)
         m = -(-maxp // c)
     recs = units * m * G
@@ -206,9 +208,9 @@ def test_workspace_bytes(lib):
     sizes = [kf.partial_attn_workspace_bytes(s, m, 513) for m in range(0, 80)]
     assert all(a <= b for a, b in zip(sizes, sizes[1:]))            # non-decreasing
     for m in range(0, 80):
-        assert sizes[m] == max(_workspace_need(k, 8, 4, 513) for k in range(0, m + 1))
-    assert _workspace_need(64, 8, 4, 513) == 256                   # 512 units: one round, unsplit
-    assert sizes[64] == _workspace_need(63, 8, 4, 513) > 256         # ... but 63 routes split
+        assert sizes[m] == max(_workspace_need(k, 8, 4, 513, 40000) for k in range(0, m + 1))
+    assert _workspace_need(64, 8, 4, 513, 40000) == 256           # 512 units: one round, unsplit
+    assert sizes[64] == _workspace_need(63, 8, 4, 513, 40000) > 256  # ... but 63 routes split
     # 1 sequence, 2 routes of 128 pages, 2 KV heads: 8 splits of 16 pages
     s = _shape(num_seqs=1, num_q_heads=8, num_kv_heads=2, num_pages=256, num_page_ids=256)
     recs = 2 * 2 * 8 * 4
@@ -216,7 +218,11 @@ def test_workspace_bytes(lib):
     # 142 routes x 8 KV heads of up to 1025 pages
     s = _shape(num_seqs=64, num_q_heads=32, num_kv_heads=8, num_pages=10, num_page_ids=10)
     assert kf.partial_attn_workspace_bytes(s, 142, 1025) == max(
-        _workspace_need(k, 8, 4, 1025) for k in range(143))
+        _workspace_need(k, 8, 4, 1025, 10) for k in range(143))
+    # a page table under 90% of routes x max pages: ragged routes, 4 ranges per slot
+    s = _shape(num_seqs=24, num_q_heads=32, num_kv_heads=8, num_pages=36000, num_page_ids=36000)
+    assert kf.partial_attn_workspace_bytes(s, 48, 1024) == max(
+        _workspace_need(k, 8, 4, 1024, 36000) for k in range(49))
     assert kf.partial_attn_workspace_bytes(s, -1, 5) == 0
     assert kf.partial_attn_workspace_bytes(_shape(head_dim=64), 4, 5) == 0
 
@@ -238,6 +244,12 @@ def test_partial_attn_plan(lib):
     fp8 = _shape(num_seqs=32, num_q_heads=64, num_kv_heads=8, kv_dtype=kf.KV_FP8_E4M3,
                  num_pages=10, num_page_ids=10)
     assert plan(fp8, 128, 1024) == (1024, 1, 1)
+    ragged = _shape(num_seqs=24, num_q_heads=32, num_kv_heads=8, num_pages=36000,
+                    num_page_ids=36000)
+    assert plan(ragged, 48, 1024) == (147, 7, 1)            # 384 units, table at 73%: ~4 per slot
+    equal = _shape(num_seqs=24, num_q_heads=32, num_kv_heads=8, num_pages=49152,
+                   num_page_ids=49152)
+    assert plan(equal, 48, 1024) == (768, 2, 1)             # full table: one round
     tiny = _shape(num_seqs=1, num_q_heads=8, num_kv_heads=2, num_pages=256, num_page_ids=256)
     assert plan(tiny, 2, 128) == (16, 8, 1)                 # 4 units: 8 splits of 16 pages
     assert plan(tiny, 2, 16) == (16, 1, 1)                  # too short to split
