@@ -66,13 +66,15 @@ ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_page
   const int64_t slots = 2 * (int64_t)cu_count();  // resident workgroups at two per CU
   const int32_t whole = max_pages_per_route > 0 ? max_pages_per_route : 1;
   if (units <= 0 || max_pages_per_route <= kMinSplitPages) return {whole, 1};
-  if (units >= slots && units % slots == 0) return {whole, 1};
+  // Ragged routes are recognised by a page table under 90% of routes x max
+  // pages (the routes' reservations sum to it).  Whole units suit equal
+  // lengths only: a ragged batch that fills whole rounds would wait for its
+  // longest unit, so it is cut into ranges like any other.
+  const bool ragged = num_page_ids * 10 < (int64_t)num_routes * max_pages_per_route * 9;
+  if (units >= slots && units % slots == 0 && !ragged) return {whole, 1};
   // Fewer units than slots: units of equal length run best as about one
-  // range per slot, one round of workgroups.  Ragged routes need more ranges
-  // for the dispatcher to balance; they are recognised by a page table
-  // under 90% of routes x max pages (the routes' reservations sum to it).
-  const bool ragged =
-      units < slots && num_page_ids * 10 < (int64_t)num_routes * max_pages_per_route * 9;
+  // range per slot, one round of workgroups; ragged routes need more ranges
+  // for the dispatcher to balance.
   const int64_t target = (units < slots ? (ragged ? 4 : 1) : 12) * slots;
   int64_t c = (units * max_pages_per_route + target - 1) / target;
   if (c < kMinSplitPages) c = kMinSplitPages;

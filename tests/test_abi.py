@@ -179,16 +179,17 @@ def test_merge_host_checks(lib):
 def _workspace_need(units_routes, H, G, maxp, num_page_ids, slots=512):
     """Bytes one launch of `units_routes` routes needs, by the planner's rule:
     units that fill whole rounds of the resident slots stay whole (no
-    records); otherwise chunks of about 12 per slot (more units than slots)
-    or about one per slot (fewer; four when the page table holds under 90%
-    of routes x max pages), never under 16 pages, an odd chunk count for the
-    longest unit except for one per slot; records of (max, sum) and o per
-    query head, each array rounded up to 256 bytes."""
+    records) unless the page table holds under 90% of routes x max pages
+    (ragged routes); otherwise chunks of about 12 per slot (more units than
+    slots) or about one per slot (fewer; four when ragged), never under 16
+    pages, an odd chunk count for the longest unit except for one per slot;
+    records of (max, sum) and o per query head, each array rounded up to 256
+    bytes."""
     rup = lambda x: -(-x // 256) * 256  # noqa: E731
     units = units_routes * H
-    if units == 0 or maxp <= 16 or (units >= slots and units % slots == 0):
+    ragged = num_page_ids * 10 < units_routes * maxp * 9
+    if units == 0 or maxp <= 16 or (units >= slots and units % slots == 0 and not ragged):
         return 256
-    ragged = units < slots and num_page_ids * 10 < units_routes * maxp * 9
     target = (12 if units >= slots else 4 if ragged else 1) * slots
     c = max(-(-units * maxp // target), 16)
     if c >= maxp:
@@ -233,16 +234,21 @@ def test_partial_attn_plan(lib):
     at most 2048 pages run two units per workgroup; fp8, route-list and
     chunked launches one."""
     s = _shape(num_seqs=16, num_q_heads=32, num_kv_heads=8, num_pages=40000, num_page_ids=40000)
+    big = _shape(num_seqs=16, num_q_heads=32, num_kv_heads=8, num_pages=200000,
+                 num_page_ids=200000)
     plan = kf.partial_attn_plan
     assert plan(s, 64, 516) == (516, 1, 2)                  # Llama layer: 512 units, unsplit
     assert plan(s, 64, 516, route_list=True) == (516, 1, 1)
-    assert plan(s, 64, 2048) == (2048, 1, 2)
-    assert plan(s, 64, 2049) == (2049, 1, 1)                # longer units: one per workgroup
-    assert plan(s, 128, 1024) == (1024, 1, 2)               # two rounds of units
+    assert plan(big, 64, 2048) == (2048, 1, 2)
+    assert plan(big, 64, 2049) == (2049, 1, 1)              # longer units: one per workgroup
+    assert plan(big, 128, 1024) == (1024, 1, 2)             # two rounds of units
+    # the same 128 routes in a page table of 40000 (31%): ragged, so ranges
+    c, m, u = plan(s, 128, 1024)
+    assert m > 1 and m % 2 == 1 and u == 1 and c * m >= 1024
     c, m, u = plan(s, 63, 516)                              # 504 units: split, combine launch
     assert m > 1 and u == 1 and c * m >= 516 and c * (m - 1) < 516
     fp8 = _shape(num_seqs=32, num_q_heads=64, num_kv_heads=8, kv_dtype=kf.KV_FP8_E4M3,
-                 num_pages=10, num_page_ids=10)
+                 num_pages=131072, num_page_ids=131072)
     assert plan(fp8, 128, 1024) == (1024, 1, 1)
     ragged = _shape(num_seqs=24, num_q_heads=32, num_kv_heads=8, num_pages=36000,
                     num_page_ids=36000)
