@@ -889,11 +889,27 @@ __global__ __launch_bounds__(64) void merge_kernel(MergeArgs a) {
     const int i = base + lane;
     const float wl = i < n ? exp2_fast((a.lse_part[(size_t)(r0 + i) * Hq + h] - M) * kLog2e) : 0.0f;
     const int cnt = min(64, n - base);
-#pragma unroll 4
-    for (int j = 0; j < cnt; ++j) {
+    const float2* ob = reinterpret_cast<const float2*>(a.o_part + ((size_t)(r0 + base) * Hq + h) * kDim) + lane;
+    const size_t rs = (size_t)Hq * kDim / 2;  // float2 elements from one route's row to the next
+    int j = 0;
+    for (; j + 4 <= cnt; j += 4) {  // four routes' loads in flight, summed in route order
+      float wr[4];
+      float2 v[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        wr[k] = __shfl(wl, j + k);
+        v[k] = ob[(j + k) * rs];
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        L += wr[k];
+        o0 += wr[k] * v[k].x;
+        o1 += wr[k] * v[k].y;
+      }
+    }
+    for (; j < cnt; ++j) {
       const float wr = __shfl(wl, j);
-      const float2 v =
-          reinterpret_cast<const float2*>(a.o_part + ((size_t)(r0 + base + j) * Hq + h) * kDim)[lane];
+      const float2 v = ob[j * rs];
       L += wr;
       o0 += wr * v.x;
       o1 += wr * v.y;
