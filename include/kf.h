@@ -133,7 +133,9 @@ int kf_kv_append(const kf_shape* shape, void* k_pool, void* v_pool, float* k_sca
  * fewer, each unit is split over several workgroups whose partials go through
  * this workspace.  The size covers every launch of at most `num_routes`
  * routes, so a workspace sized for a route table also serves
- * kf_partial_attn_subset over any part of it.  No initialisation is needed;
+ * kf_partial_attn_subset over any part of it, and it covers ragged and
+ * equal routes alike: it does not depend on shape->num_page_ids, so it stays
+ * valid as the page table grows or shrinks.  No initialisation is needed;
  * contents are dead between calls.  Returns 0 for invalid arguments.
  */
 size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes,
@@ -151,6 +153,11 @@ size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes
  *   *max_chunks   most ranges per unit; 1 = every unit whole, no combine
  *                 launch and no workspace use
  *   *units_per_wg 1 or 2 (route, KV head) units per workgroup
+ * The plan reads the launch size, the KV heads and dtype, the device's
+ * compute units, max_pages_per_route and shape->num_page_ids: a page table
+ * under 90% of num_launch * max_pages_per_route marks the routes as ragged,
+ * and ragged routes are cut into more ranges.  A max_pages_per_route far
+ * above the longest route therefore costs speed, never correctness.
  * Host only; launches nothing.  Any output pointer may be NULL.  Returns
  * KF_OK, KF_ERR_INVALID_ARG (null or invalid shape, negative sizes,
  * route_list_launch not 0 or 1) or KF_ERR_UNSUPPORTED (a shape or size the

@@ -152,13 +152,16 @@ size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes
   const int32_t group = shape->num_q_heads / shape->num_kv_heads;
   // The largest need of any launch of at most num_routes routes: fewer routes
   // may not fill the GPU and then split their units, so a workspace sized for
-  // a whole route table must also serve a launch over a subset of it.
+  // a whole route table must also serve a launch over a subset of it.  Both
+  // readings of the page table (ragged routes or not) are covered, so the
+  // size does not depend on shape->num_page_ids, which grows with the table.
   size_t most = 0;
   for (int32_t m = num_routes > 0 ? 1 : 0; m <= num_routes; ++m) {
-    const kf::ChunkPlan plan = kf::plan_chunks(m, shape->num_kv_heads, max_pages_per_route,
-                                               shape->num_page_ids);
-    const size_t t = kf::workspace_layout(m, shape->num_kv_heads, group, plan.max_chunks).total;
-    if (t > most) most = t;
+    for (const int64_t pids : {(int64_t)0, INT64_MAX}) {
+      const kf::ChunkPlan plan = kf::plan_chunks(m, shape->num_kv_heads, max_pages_per_route, pids);
+      const size_t t = kf::workspace_layout(m, shape->num_kv_heads, group, plan.max_chunks).total;
+      if (t > most) most = t;
+    }
   }
   return most;
 }

@@ -176,18 +176,17 @@ def test_merge_host_checks(lib):
     assert lib.kf_merge_partials(0, 4, 8, 128, *([None] * 7), None) == 0
 
 
-def _workspace_need(units_routes, H, G, maxp, num_page_ids, slots=512):
+def _workspace_need(units_routes, H, G, maxp, ragged, slots=512):
     """Bytes one launch of `units_routes` routes needs, by the planner's rule:
     units that fill whole rounds of the resident slots stay whole (no
-    records) unless the page table holds under 90% of routes x max pages
-    (ragged routes); otherwise chunks of about 12 per slot (more units than
+    records) unless the routes are ragged (a page table under 90% of routes
+    x max pages); otherwise chunks of about 12 per slot (more units than
     slots) or about one per slot (fewer; four when ragged), never under 16
     pages, an odd chunk count for the longest unit except for one per slot;
     records of (max, sum) and o per query head, each array rounded up to 256
     bytes."""
     rup = lambda x: -(-x // 256) * 256  # noqa: E731
     units = units_routes * H
-    ragged = num_page_ids * 10 < units_routes * maxp * 9
     if units == 0 or maxp <= 16 or (units >= slots and units % slots == 0 and not ragged):
         return 256
     target = (12 if units >= slots else 4 if ragged else 1) * slots
@@ -208,22 +207,23 @@ def test_workspace_bytes(lib):
     s = _shape(num_seqs=16, num_q_heads=32, num_kv_heads=8, num_pages=40000, num_page_ids=40000)
     sizes = [kf.partial_attn_workspace_bytes(s, m, 513) for m in range(0, 80)]
     assert all(a <= b for a, b in zip(sizes, sizes[1:]))            # non-decreasing
+    need = lambda k, maxp: max(_workspace_need(k, 8, 4, maxp, rg) for rg in (False, True))  # noqa: E731
     for m in range(0, 80):
-        assert sizes[m] == max(_workspace_need(k, 8, 4, 513, 40000) for k in range(0, m + 1))
-    assert _workspace_need(64, 8, 4, 513, 40000) == 256           # 512 units: one round, unsplit
-    assert sizes[64] == _workspace_need(63, 8, 4, 513, 40000) > 256  # ... but 63 routes split
+        assert sizes[m] == max(need(k, 513) for k in range(0, m + 1))
+    assert _workspace_need(64, 8, 4, 513, False) == 256           # 512 equal units: unsplit
+    assert _workspace_need(64, 8, 4, 513, True) > 256             # ... ragged ones are cut
+    assert _workspace_need(63, 8, 4, 513, False) > 256            # 63 routes split either way
     # 1 sequence, 2 routes of 128 pages, 2 KV heads: 8 splits of 16 pages
     s = _shape(num_seqs=1, num_q_heads=8, num_kv_heads=2, num_pages=256, num_page_ids=256)
     recs = 2 * 2 * 8 * 4
     assert kf.partial_attn_workspace_bytes(s, 2, 128) == 1024 + recs * 128 * 4
     # 142 routes x 8 KV heads of up to 1025 pages
     s = _shape(num_seqs=64, num_q_heads=32, num_kv_heads=8, num_pages=10, num_page_ids=10)
-    assert kf.partial_attn_workspace_bytes(s, 142, 1025) == max(
-        _workspace_need(k, 8, 4, 1025, 10) for k in range(143))
-    # a page table under 90% of routes x max pages: ragged routes, 4 ranges per slot
-    s = _shape(num_seqs=24, num_q_heads=32, num_kv_heads=8, num_pages=36000, num_page_ids=36000)
-    assert kf.partial_attn_workspace_bytes(s, 48, 1024) == max(
-        _workspace_need(k, 8, 4, 1024, 36000) for k in range(49))
+    assert kf.partial_attn_workspace_bytes(s, 142, 1025) == max(need(k, 1025) for k in range(143))
+    # the size does not depend on the page table's size
+    for pids in (10, 36000, 10 ** 9):
+        s = _shape(num_seqs=24, num_q_heads=32, num_kv_heads=8, num_pages=10, num_page_ids=pids)
+        assert kf.partial_attn_workspace_bytes(s, 48, 1024) == max(need(k, 1024) for k in range(49))
     assert kf.partial_attn_workspace_bytes(s, -1, 5) == 0
     assert kf.partial_attn_workspace_bytes(_shape(head_dim=64), 4, 5) == 0
 
