@@ -61,7 +61,7 @@ int cu_count() {
 }  // namespace
 
 ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_pages_per_route,
-                      int64_t num_page_ids) {
+                      int64_t num_page_ids, bool fp8) {
   const int64_t units = (int64_t)num_routes * num_kv_heads;
   const int64_t slots = 2 * (int64_t)cu_count();  // resident workgroups at two per CU
   const int32_t whole = max_pages_per_route > 0 ? max_pages_per_route : 1;
@@ -74,8 +74,11 @@ ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_page
   if (units >= slots && units % slots == 0 && !ragged) return {whole, 1};
   // Fewer units than slots: units of equal length run best as about one
   // range per slot, one round of workgroups; ragged routes need more ranges
-  // for the dispatcher to balance.
-  const int64_t target = (units < slots ? (ragged ? 4 : 1) : 12) * slots;
+  // for the dispatcher to balance.  More units than slots: about 12 ranges
+  // per slot, 6 for fp8 pools, whose pages hold half the bytes, so that a
+  // workgroup streams about as much either way.
+  const int64_t many = fp8 ? 6 : 12;
+  const int64_t target = (units < slots ? (ragged ? 4 : 1) : many) * slots;
   int64_t c = (units * max_pages_per_route + target - 1) / target;
   if (c < kMinSplitPages) c = kMinSplitPages;
   if (c >= max_pages_per_route) return {whole, 1};
@@ -150,6 +153,7 @@ size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes
                                        int32_t max_pages_per_route) {
   if (check_shape(shape) != KF_OK || num_routes < 0 || max_pages_per_route < 0) return 0;
   const int32_t group = shape->num_q_heads / shape->num_kv_heads;
+  const bool fp8 = shape->kv_dtype == KF_KV_FP8_E4M3;
   // The largest need of any launch of at most num_routes routes: fewer routes
   // may not fill the GPU and then split their units, so a workspace sized for
   // a whole route table must also serve a launch over a subset of it.  Both
@@ -158,7 +162,8 @@ size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes
   size_t most = 0;
   for (int32_t m = num_routes > 0 ? 1 : 0; m <= num_routes; ++m) {
     for (const int64_t pids : {(int64_t)0, INT64_MAX}) {
-      const kf::ChunkPlan plan = kf::plan_chunks(m, shape->num_kv_heads, max_pages_per_route, pids);
+      const kf::ChunkPlan plan =
+          kf::plan_chunks(m, shape->num_kv_heads, max_pages_per_route, pids, fp8);
       const size_t t = kf::workspace_layout(m, shape->num_kv_heads, group, plan.max_chunks).total;
       if (t > most) most = t;
     }
@@ -175,7 +180,8 @@ int kf_partial_attn_plan(const kf_shape* shape, int32_t num_launch, int32_t max_
     return KF_ERR_INVALID_ARG;
   if (num_launch > 65535 || shape->num_kv_heads > 65535) return KF_ERR_UNSUPPORTED;
   const kf::ChunkPlan plan = kf::plan_chunks(num_launch, shape->num_kv_heads, max_pages_per_route,
-                                             shape->num_page_ids);
+                                             shape->num_page_ids,
+                                             shape->kv_dtype == KF_KV_FP8_E4M3);
   if (chunk_pages) *chunk_pages = plan.chunk_pages;
   if (max_chunks) *max_chunks = plan.max_chunks;
   if (units_per_wg)
@@ -250,7 +256,8 @@ int prepare_partial(const kf_shape* shape, const void* q, const void* k_pool, co
     if (p && !aligned(p, 4)) return KF_ERR_INVALID_ARG;
   const int32_t group = shape->num_q_heads / shape->num_kv_heads;
   const kf::ChunkPlan plan = kf::plan_chunks(num_launch, shape->num_kv_heads, max_pages_per_route,
-                                             shape->num_page_ids);
+                                             shape->num_page_ids,
+                                             shape->kv_dtype == KF_KV_FP8_E4M3);
   const kf::WorkspaceLayout l =
       kf::workspace_layout(num_launch, shape->num_kv_heads, group, plan.max_chunks);
   if (!workspace || !aligned(workspace, 256) || workspace_bytes < l.total) return KF_ERR_WORKSPACE;

@@ -90,14 +90,14 @@ struct WorkspaceLayout {
 // One workgroup owns a whole unit when the units fill whole rounds of the
 // GPU's resident workgroups (two per compute unit); otherwise units are cut
 // into chunks of chunk_pages pages, so the dispatcher balances uneven routes,
-// and a combine kernel follows: about 12 chunks per resident slot when units
-// outnumber slots, else about one (four when the page table shows ragged
+// and a combine kernel follows: about 12 chunks per resident slot (6 for
+// fp8) when units outnumber slots, else about one (four when the page table shows ragged
 // routes), an odd number of chunks for the longest unit where it matters.
 struct ChunkPlan {
   int32_t chunk_pages, max_chunks;
 };
 ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_pages_per_route,
-                      int64_t num_page_ids);
+                      int64_t num_page_ids, bool fp8);
 // Units per workgroup of a partial-attention launch of num_launch routes
 // (1 or 2); route_list: a launch over a route list (kf_partial_attn_subset).
 int32_t units_per_workgroup(bool fp8, bool route_list, const ChunkPlan& plan, int32_t num_launch,

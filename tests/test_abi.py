@@ -176,12 +176,13 @@ def test_merge_host_checks(lib):
     assert lib.kf_merge_partials(0, 4, 8, 128, *([None] * 7), None) == 0
 
 
-def _workspace_need(units_routes, H, G, maxp, ragged, slots=512):
+def _workspace_need(units_routes, H, G, maxp, ragged, slots=512, fp8=False):
     """Bytes one launch of `units_routes` routes needs, by the planner's rule:
     units that fill whole rounds of the resident slots stay whole (no
     records) unless the routes are ragged (a page table under 90% of routes
     x max pages); otherwise chunks of about 12 per slot (more units than
-    slots) or about one per slot (fewer; four when ragged), never under 16
+    slots; 6 for fp8 pools) or about one per slot (fewer; four when ragged),
+    never under 16
     pages, an odd chunk count for the longest unit except for one per slot;
     records of (max, sum) and o per query head, each array rounded up to 256
     bytes."""
@@ -189,7 +190,7 @@ def _workspace_need(units_routes, H, G, maxp, ragged, slots=512):
     units = units_routes * H
     if units == 0 or maxp <= 16 or (units >= slots and units % slots == 0 and not ragged):
         return 256
-    target = (12 if units >= slots else 4 if ragged else 1) * slots
+    target = ((6 if fp8 else 12) if units >= slots else 4 if ragged else 1) * slots
     c = max(-(-units * maxp // target), 16)
     if c >= maxp:
         return 256
@@ -250,6 +251,17 @@ def test_partial_attn_plan(lib):
     fp8 = _shape(num_seqs=32, num_q_heads=64, num_kv_heads=8, kv_dtype=kf.KV_FP8_E4M3,
                  num_pages=131072, num_page_ids=131072)
     assert plan(fp8, 128, 1024) == (1024, 1, 1)
+    fp8t = _shape(num_seqs=20, num_q_heads=64, num_kv_heads=8, kv_dtype=kf.KV_FP8_E4M3,
+                  num_pages=81920, num_page_ids=81920)
+    bf16t = _shape(num_seqs=20, num_q_heads=64, num_kv_heads=8, num_pages=81920,
+                   num_page_ids=81920)
+    assert plan(fp8t, 80, 1024) == (214, 5, 1)               # 640 units: ~6 ranges per slot
+    assert plan(bf16t, 80, 1024) == (94, 11, 1)              # ... and ~12 for bf16
+    for pids in (100, 81920):
+        sh = _shape(num_seqs=20, num_q_heads=64, num_kv_heads=8, kv_dtype=kf.KV_FP8_E4M3,
+                    num_pages=10, num_page_ids=pids)
+        assert kf.partial_attn_workspace_bytes(sh, 80, 1024) == max(
+            _workspace_need(k, 8, 8, 1024, rg, fp8=True) for k in range(81) for rg in (False, True))
     ragged = _shape(num_seqs=24, num_q_heads=32, num_kv_heads=8, num_pages=36000,
                     num_page_ids=36000)
     assert plan(ragged, 48, 1024) == (147, 7, 1)            # 384 units, table at 73%: ~4 per slot
