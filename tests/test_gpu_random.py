@@ -55,3 +55,24 @@ def test_random_shape(gpu, case):
     o = run_oracle(inst, steps)
     g = host(run_gpu(inst, steps, fused=bool(inst.wl.appends)))
     compare_all(g, o)
+
+
+@pytest.mark.parametrize("ragged", [True, False])
+def test_full_round_of_units_ragged_or_equal(gpu, ragged):
+    """512 units (64 single-route sequences x 8 KV heads) fill whole rounds of
+    the resident slots.  Equal routes stay whole, two units per workgroup;
+    ragged ones (a page table well under routes x max pages) are cut into
+    page ranges.  Both match the oracle over fused steps."""
+    from paper_2606_29207_amd import kf
+    from paper_2606_29207_amd.step import DecodeState
+    rng = np.random.default_rng(606)
+    lens = [int(x) for x in rng.integers(16, 900, 64)] if ragged else [700] * 64
+    wl = workload("llama8b_32k", num_seqs=64, part_tokens=1 << 20, appends=1)
+    inst = make_instance(wl, seed=31, steps=2, seq_lens=lens)
+    assert len(inst.routes) * wl.num_kv_heads == 512
+    st = DecodeState.from_instance(inst)
+    _, max_chunks, units = kf.partial_attn_plan(st.shape, st.routes.shape[0], st.max_pages_per_route)
+    assert (max_chunks > 1 and units == 1) if ragged else (max_chunks == 1 and units == 2)
+    del st
+    o = run_oracle(inst, 2)
+    compare_all(host(run_gpu(inst, 2, fused=True)), o)
