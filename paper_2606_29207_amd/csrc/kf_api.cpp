@@ -92,6 +92,15 @@ ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_page
     c = (max_pages_per_route + m) / (m + 1);
     if (c < kMinSplitPages) c = kMinSplitPages;
     m = (max_pages_per_route + c - 1) / c;
+    // with many ranges the rounding can keep the count even: shorten the
+    // ranges until it is odd (or the 16-page floor is reached)
+    for (int64_t cc = c - 1; m % 2 == 0 && cc >= kMinSplitPages; --cc) {
+      const int64_t mm = (max_pages_per_route + cc - 1) / cc;
+      if (mm % 2 == 1) {
+        c = cc;
+        m = mm;
+      }
+    }
   }
   if (m > 65535) {
     m = 65535;

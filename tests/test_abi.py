@@ -198,6 +198,11 @@ def _workspace_need(units_routes, H, G, maxp, ragged, slots=512, fp8=False):
     if (units >= slots or ragged) and m % 2 == 0:
         c = max(-(-maxp // (m + 1)), 16)
         m = -(-maxp // c)
+        cc = c - 1
+        while m % 2 == 0 and cc >= 16:
+            if -(-maxp // cc) % 2 == 1:
+                c, m = cc, -(-maxp // cc)
+            cc -= 1
     recs = units * m * G
     return rup(recs * 2 * 4) + rup(recs * 128 * 4)
 
@@ -323,3 +328,39 @@ def test_binding_refuses_host_tensors_and_bad_shapes(lib):
     with pytest.raises(kf.KFError, match="device tensor"):
         kf.decode_step(s, q, pool, pool, q[:, :2], q[:, :2], routes, flags, 1, pids,
                        torch.zeros(2, dtype=torch.int32), o, lse, o, lse, ws, flags)
+
+
+def test_plan_invariants_over_random_shapes(lib):
+    """Planner invariants for 3000 seeded random launches (256 compute units
+    assumed): the ranges cover the longest unit, no range is under 16 pages
+    unless the unit stays whole, the range count is odd when units outnumber
+    slots or the routes are ragged (unless ranges hit the 16-page floor), two
+    units per workgroup only for unsplit bf16 launches over the whole table,
+    and the workspace sized for the table covers the launch under any page
+    table size."""
+    import numpy as np
+    rng = np.random.default_rng(2606)
+    for _ in range(3000):
+        hkv = int(rng.choice([1, 2, 4, 8, 16]))
+        group = int(rng.integers(1, 17))
+        dtype = kf.KV_FP8_E4M3 if rng.random() < 0.3 else kf.KV_BF16
+        routes = int(rng.integers(1, 3000))
+        maxp = int(rng.integers(1, 5000))
+        pids = int(rng.integers(1, routes * maxp + 1))
+        s = _shape(num_seqs=4, num_q_heads=group * hkv, num_kv_heads=hkv, kv_dtype=dtype,
+                   num_pages=10, num_page_ids=pids)
+        launch = int(rng.integers(1, routes + 1))
+        listed = bool(rng.random() < 0.3)
+        c, m, u = kf.partial_attn_plan(s, launch, maxp, listed)
+        assert c * m >= maxp and (m == 1 or c * (m - 1) < maxp)
+        assert m == 1 or c >= 16
+        units = launch * hkv
+        ragged = pids * 10 < launch * maxp * 9
+        if m > 1 and (units >= 512 or ragged) and c > 16:
+            assert m % 2 == 1, (units, maxp, pids, c, m)
+        if u == 2:
+            assert m == 1 and dtype == kf.KV_BF16 and not listed and units >= 512 and maxp <= 2048
+        need = 256 if m == 1 else -(-units * m * group * 2 * 4 // 256) * 256 + \
+            -(-units * m * group * 128 * 4 // 256) * 256
+        if routes <= 200:   # the sizing loop is linear in the table's routes
+            assert kf.partial_attn_workspace_bytes(s, routes, maxp) >= need
