@@ -219,6 +219,8 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=40)
     ap.add_argument("--workload", default="llama8b_32k")
+    ap.add_argument("--kv-layout", choices=("page", "head"), default="page",
+                    help="pool layout: page-major [P][Hkv][...] (default) or head-major [Hkv][P][...]")
     ap.add_argument("--seed", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB")
@@ -254,7 +256,9 @@ def main(argv=None):
     import torch
     from paper_2606_29207_amd.step import DecodeState
     torch.cuda.set_device(0)
-    st = DecodeState.from_instance(inst)
+    from paper_2606_29207_amd import kf as _kf
+    st = DecodeState.from_instance(
+        inst, kv_layout=_kf.KV_HEAD_MAJOR if args.kv_layout == "head" else _kf.KV_PAGE_MAJOR)
     news = [st.upload_new_tokens(*inst.new_tokens(s)) if wl.appends else (None, None)
             for s in range(W + 3 * K)]
     stream = torch.cuda.current_stream()
@@ -366,7 +370,8 @@ def main(argv=None):
     am_b = np.mean([b["partial"] + b["merge"] for b in by2])
     us_step = wall / K * 1e6
     achieved = par_b / (t_par.mean() * 1e-6) / 1e9
-    traffic = counter_traffic(wl.name, args.seed)
+    # the committed counter profiles were taken on page-major pools
+    traffic = counter_traffic(wl.name, args.seed) if args.kv_layout == "page" else None
     out = {
         "metric": METRIC,
         "value": round(step_b / (us_step * 1e-6) / 1e9, 2),
@@ -385,7 +390,8 @@ def main(argv=None):
                    "kv_heads": wl.num_kv_heads, "head_dim": wl.head_dim,
                    "context": int(inst.seq_lens.max()), "route_tokens": wl.part_tokens,
                    "routes": int(len(inst.routes)), "page_tokens": 16,
-                   "appends_per_step": wl.appends, "kv_dtype": wl.kv_dtype},
+                   "appends_per_step": wl.appends, "kv_dtype": wl.kv_dtype,
+                   "kv_layout": args.kv_layout},
         "schedule": "fused" if fused else "serial",
         "breakdown_pass": "a second run of K steps as three calls with HIP events around each",
         "breakdown_us": {"append": round(float(t_app.mean()), 2) if wl.appends else None,

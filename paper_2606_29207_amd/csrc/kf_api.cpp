@@ -25,6 +25,7 @@ int check_shape(const kf_shape* s) {
   if (s->num_q_heads / s->num_kv_heads > KF_MAX_GROUP) return KF_ERR_UNSUPPORTED;
   if (s->head_dim != KF_HEAD_DIM || s->page_size != KF_PAGE_SIZE) return KF_ERR_UNSUPPORTED;
   if (s->kv_dtype != KF_KV_BF16 && s->kv_dtype != KF_KV_FP8_E4M3) return KF_ERR_UNSUPPORTED;
+  if (s->kv_layout != KF_KV_PAGE_MAJOR && s->kv_layout != KF_KV_HEAD_MAJOR) return KF_ERR_UNSUPPORTED;
   if (!isfinite(s->scale)) return KF_ERR_INVALID_ARG;
   // element offsets of the pools are formed in 64 bits; the grid needs
   // num_kv_heads <= 65535 (checked per call together with num_routes)
@@ -237,6 +238,7 @@ int prepare_append(const kf_shape* shape, void* k_pool, void* v_pool, float* k_s
   a.num_routes = num_routes;
   a.num_pages = shape->num_pages;
   a.num_page_ids = shape->num_page_ids;
+  a.head_major = shape->kv_layout == KF_KV_HEAD_MAJOR;
   return KF_OK;
 }
 
@@ -298,6 +300,7 @@ int prepare_partial(const kf_shape* shape, const void* q, const void* k_pool, co
                                            shape->num_kv_heads, max_pages_per_route);
   a.num_pages = shape->num_pages;
   a.num_page_ids = shape->num_page_ids;
+  a.head_major = shape->kv_layout == KF_KV_HEAD_MAJOR;
   a.scale_log2 = (float)((double)shape->scale * 1.4426950408889634074);
   return KF_OK;
 }
@@ -423,6 +426,7 @@ int kf_debug_gather(const kf_shape* shape, const void* k_pool, const void* v_poo
   a.max_pages_per_route = max_pages_per_route;
   a.num_pages = shape->num_pages;
   a.num_page_ids = shape->num_page_ids;
+  a.head_major = shape->kv_layout == KF_KV_HEAD_MAJOR;
   return kf::launch_gather(a, shape->kv_dtype == KF_KV_FP8_E4M3, route, max_tokens, out_k, out_v,
                            as_stream(stream)) == hipSuccess
              ? KF_OK

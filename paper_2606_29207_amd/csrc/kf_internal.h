@@ -30,6 +30,7 @@ struct AppendArgs {
   const int32_t* page_ids;
   int32_t* err_flags;
   int32_t num_seqs, num_kv_heads, num_routes, num_pages, num_page_ids;
+  int32_t head_major;  // pools [Hkv][num_pages][...] instead of [num_pages][Hkv][...]
 };
 
 struct PartialArgs {
@@ -51,6 +52,7 @@ struct PartialArgs {
   int32_t num_units_routes;  // routes launched: num_list, or num_routes without a list
   int32_t chunk_pages, max_chunks;  // a unit of n pages uses ceil(n / chunk_pages) workgroups
   int32_t units_per_wg;  // 2: unsplit bf16 launch, two units per 512-thread workgroup
+  int32_t head_major;    // pools [Hkv][num_pages][...] instead of [num_pages][Hkv][...]
   int32_t num_pages, num_page_ids;
   float scale_log2;     // scale * log2(e): scores are kept in the base-2 domain
   // Fused tail append (kf_decode_step; all NULL otherwise): the route that is

@@ -41,6 +41,12 @@
 namespace kf {
 namespace {
 
+// Slice index of (page, KV head) in a pool: page-major pools are
+// [num_pages][Hkv][...], head-major ones [Hkv][num_pages][...].
+__device__ __forceinline__ size_t pool_slice(int page, int g, int H, int P, int32_t head_major) {
+  return head_major ? (size_t)g * P + page : (size_t)page * H + g;
+}
+
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -197,7 +203,7 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
     uint16_t* vp = static_cast<uint16_t*>(a.v_pool);
     for (int e = threadIdx.x; e < H * kDim; e += blockDim.x) {
       const int g = e / kDim, d = e % kDim;
-      const size_t head = (size_t)pid * H + g;
+      const size_t head = pool_slice(pid, g, H, a.num_pages, a.head_major);
       const uint16_t kv = a.k_new[((size_t)b * H + g) * kDim + d];
       const uint16_t vv = a.v_new[((size_t)b * H + g) * kDim + d];
       kp[(head * kPage + slot) * kDim + d] = kv;
@@ -211,7 +217,7 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
       const bool is_v = pr & 1;
       float* scale = (is_v ? a.v_scale : a.k_scale) + (size_t)pid * H + g;
       uint8_t* page = static_cast<uint8_t*>(is_v ? a.v_pool : a.k_pool) +
-                      ((size_t)pid * H + g) * (kPage * kDim);
+                      pool_slice(pid, g, H, a.num_pages, a.head_major) * (kPage * kDim);
       const float s_new = append_e4m3_head(page, *scale, slot, is_v,
                                            (is_v ? a.v_new : a.k_new) + ((size_t)b * H + g) * kDim,
                                            lane);
@@ -276,7 +282,7 @@ __device__ __forceinline__ void store_new_token(const PartialArgs& a, const Rout
   const int H = a.num_kv_heads;
   const uint16_t* kn = a.k_new + ((size_t)rv.seq * H + g) * kDim;
   const uint16_t* vn = a.v_new + ((size_t)rv.seq * H + g) * kDim;
-  const size_t head = (size_t)rv.app_pid * H + g;
+  const size_t head = pool_slice(rv.app_pid, g, H, a.num_pages, a.head_major);
   if constexpr (!FP8) {
     if (tid < kDim) {
       static_cast<uint16_t*>(a.k_pool_w)[(head * kPage + rv.app_slot) * kDim + tid] = kn[tid];
@@ -286,7 +292,8 @@ __device__ __forceinline__ void store_new_token(const PartialArgs& a, const Rout
     const int wv = tid >> 6, lane = tid & 63;
     if (wv < 2) {
       const bool is_v = wv == 1;
-      float* scale = (is_v ? a.v_scale_w : a.k_scale_w) + head;
+      // scales are [num_pages][Hkv] in either pool layout
+      float* scale = (is_v ? a.v_scale_w : a.k_scale_w) + (size_t)rv.app_pid * H + g;
       uint8_t* page = static_cast<uint8_t*>(is_v ? a.v_pool_w : a.k_pool_w) + head * (kPage * kDim);
       const float s_new = append_e4m3_head(page, *scale, rv.app_slot, is_v, is_v ? vn : kn, lane);
       if (lane == 0) {
@@ -358,7 +365,7 @@ __device__ __forceinline__ T pick4(T v0, T v1, T v2, T v3, int i) {
 // second, one workgroup per CU, so both units of a CU start at once.  In
 // that mode all 512 threads reach every barrier: a half without work (no
 // unit, a bad or empty one) skips its work, never the barriers.
-template <bool FP8, int UPW>
+template <bool FP8, int UPW, bool HM>
 __global__ __launch_bounds__(kThreads * UPW, 2 / UPW) void partial_kernel(PartialArgs a) {
   using GeoT = Geo<FP8>;
   constexpr int TP = GeoT::TP, NC = GeoT::NC, NH = GeoT::NH;
@@ -509,8 +516,8 @@ __global__ __launch_bounds__(kThreads * UPW, 2 / UPW) void partial_kernel(Partia
   auto issue = [&](TileRaw<FP8>& t, const TileInfo& ti) {
     const int pk = pick4(ti.pid0, ti.pid1, ti.pid2, ti.pid3, kpage);
     const int pv = pick4(ti.pid0, ti.pid1, ti.pid2, ti.pid3, vpage);
-    const size_t hk = ((size_t)pk * H + g) * head_elems;
-    const size_t hv = ((size_t)pv * H + g) * head_elems;
+    const size_t hk = (HM ? (size_t)g * a.num_pages + pk : (size_t)pk * H + g) * head_elems;
+    const size_t hv = (HM ? (size_t)g * a.num_pages + pv : (size_t)pv * H + g) * head_elems;
     if constexpr (!FP8) {
       const uint16_t* kb = static_cast<const uint16_t*>(a.k_pool) + hk + koff;
       const uint16_t* vb = static_cast<const uint16_t*>(a.v_pool) + hv + voff;
@@ -817,7 +824,7 @@ __global__ __launch_bounds__(256) void gather_kernel(PartialArgs a, int route, i
     const int g = e / (kPage * kDim), slot = (e / kDim) % kPage, d = e % kDim;
     const int j = p * kPage + slot;
     if (j >= n) continue;
-    const size_t head = (size_t)pid * H + g;
+    const size_t head = pool_slice(pid, g, H, a.num_pages, a.head_major);
     out_k[((size_t)j * H + g) * kDim + d] = kp[(head * kPage + slot) * kDim + d];
     out_v[((size_t)j * H + g) * kDim + d] = vp[(head * kDim + d) * kPage + slot];
   }
@@ -919,6 +926,17 @@ __global__ __launch_bounds__(64) void merge_kernel(MergeArgs a) {
   if (lane == 0) *lse_out = M + __logf(L);
 }
 
+template <bool FP8, int UPW>
+hipError_t launch_partial_kernel(const PartialArgs& a, dim3 grid, hipStream_t stream) {
+  if (a.head_major)
+    hipLaunchKernelGGL(HIP_KERNEL_NAME(partial_kernel<FP8, UPW, true>), grid, dim3(kThreads * UPW), 0,
+                       stream, a);
+  else
+    hipLaunchKernelGGL(HIP_KERNEL_NAME(partial_kernel<FP8, UPW, false>), grid, dim3(kThreads * UPW), 0,
+                       stream, a);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_append(const AppendArgs& a, bool fp8, hipStream_t stream) {
@@ -932,18 +950,12 @@ hipError_t launch_append(const AppendArgs& a, bool fp8, hipStream_t stream) {
 
 hipError_t launch_partial(const PartialArgs& a, bool fp8, hipStream_t stream) {
   if (a.num_units_routes == 0) return hipSuccess;
-  if (!fp8 && a.units_per_wg == 2) {
-    const dim3 grid(1, a.num_kv_heads, (a.num_units_routes + 1) / 2);
-    hipLaunchKernelGGL(HIP_KERNEL_NAME(partial_kernel<false, 2>), grid, dim3(2 * kThreads), 0,
-                       stream, a);
-    return hipGetLastError();
-  }
+  if (!fp8 && a.units_per_wg == 2)
+    return launch_partial_kernel<false, 2>(a, dim3(1, a.num_kv_heads, (a.num_units_routes + 1) / 2),
+                                           stream);
   const dim3 grid(a.max_chunks, a.num_kv_heads, a.num_units_routes);
-  if (fp8)
-    hipLaunchKernelGGL(HIP_KERNEL_NAME(partial_kernel<true, 1>), grid, dim3(kThreads), 0, stream, a);
-  else
-    hipLaunchKernelGGL(HIP_KERNEL_NAME(partial_kernel<false, 1>), grid, dim3(kThreads), 0, stream, a);
-  hipError_t e = hipGetLastError();
+  hipError_t e = fp8 ? launch_partial_kernel<true, 1>(a, grid, stream)
+                     : launch_partial_kernel<false, 1>(a, grid, stream);
   if (e != hipSuccess || a.max_chunks == 1) return e;
   hipLaunchKernelGGL(combine_kernel, dim3(a.num_kv_heads, a.num_units_routes), dim3(kThreads), 0,
                      stream, a);

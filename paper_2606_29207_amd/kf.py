@@ -31,6 +31,8 @@ ERR_HOST_MEMORY = -7
 EFLAG_TAIL_FULL = 1
 EFLAG_BAD_ROUTE = 2
 EFLAG_BAD_PAGE = 4
+KV_PAGE_MAJOR = 0
+KV_HEAD_MAJOR = 1
 
 # every symbol include/kf.h declares
 EXPORTS = ("kf_kv_append", "kf_partial_attn_workspace_bytes", "kf_partial_attn_plan",
@@ -52,7 +54,7 @@ class Shape(ctypes.Structure):
                 ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("page_size", ctypes.c_int32), ("kv_dtype", ctypes.c_int32),
                 ("num_pages", ctypes.c_int32), ("num_page_ids", ctypes.c_int32),
-                ("scale", ctypes.c_float)]
+                ("scale", ctypes.c_float), ("kv_layout", ctypes.c_int32)]
 
 
 _lib = None
@@ -147,19 +149,23 @@ def _check_tables(shape: Shape, k_pool, v_pool, routes, page_ids):
 
 
 def make_shape(num_seqs, num_q_heads, num_kv_heads, kv_dtype, num_pages, num_page_ids,
-               scale) -> Shape:
+               scale, kv_layout=None) -> Shape:
     return Shape(num_seqs, num_q_heads, num_kv_heads, HEAD_DIM, PAGE_SIZE, kv_dtype,
-                 num_pages, num_page_ids, float(scale))
+                 num_pages, num_page_ids, float(scale),
+                 KV_PAGE_MAJOR if kv_layout is None else kv_layout)
 
 
 def _pool_dtype(k_pool: torch.Tensor) -> int:
     return KV_FP8_E4M3 if k_pool.element_size() == 1 else KV_BF16
 
 
-def shape_of(q, k_pool, page_ids, scale) -> Shape:
-    """kf_shape from q [B, Hq, 128], K pool [P, Hkv, 16, 128] and page_ids."""
-    return make_shape(q.shape[0], q.shape[1], k_pool.shape[1], _pool_dtype(k_pool),
-                      k_pool.shape[0], page_ids.numel(), scale)
+def shape_of(q, k_pool, page_ids, scale, kv_layout=None) -> Shape:
+    """kf_shape from q [B, Hq, 128], the K pool ([P, Hkv, 16, 128] page-major,
+    [Hkv, P, 16, 128] head-major) and page_ids."""
+    head_major = kv_layout == KV_HEAD_MAJOR
+    P, H = (k_pool.shape[1], k_pool.shape[0]) if head_major else (k_pool.shape[0], k_pool.shape[1])
+    return make_shape(q.shape[0], q.shape[1], H, _pool_dtype(k_pool), P, page_ids.numel(), scale,
+                      kv_layout)
 
 
 def kv_append(shape: Shape, k_pool, v_pool, k_new, v_new, routes, tail_route, page_ids,

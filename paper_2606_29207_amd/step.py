@@ -30,15 +30,21 @@ class DecodeState:
     Arrays follow include/kf.h: q uint16 (bf16 bits) [B, Hq, 128]; pools
     uint16 or uint8 (E4M3 codes) [P, Hkv, 16, 128] / [P, Hkv, 128, 16];
     scales float32 [P, Hkv] or None; routes int32 [R, 6]; page_ids int32;
-    seq_route_begin int32 [B+1]; tail_route int32 [B].
+    seq_route_begin int32 [B+1]; tail_route int32 [B].  kv_layout =
+    kf.KV_HEAD_MAJOR stores the (page-major) pools given here head-major on
+    the device: [Hkv, P, ...].
     """
 
     def __init__(self, *, q, k_pool, v_pool, routes, page_ids, seq_route_begin, tail_route,
-                 scale, max_pages_per_route, k_scale=None, v_scale=None, device="cuda"):
+                 scale, max_pages_per_route, k_scale=None, v_scale=None, device="cuda",
+                 kv_layout=None):
         self.device = torch.device(device)
+        self.kv_layout = kf.KV_PAGE_MAJOR if kv_layout is None else kv_layout
+        relayout = ((lambda x: np.ascontiguousarray(np.swapaxes(x, 0, 1)))
+                    if self.kv_layout == kf.KV_HEAD_MAJOR else (lambda x: x))
         self.q = _to_dev(q, device)
-        self.k_pool = _to_dev(k_pool, device)
-        self.v_pool = _to_dev(v_pool, device)
+        self.k_pool = _to_dev(relayout(k_pool), device)
+        self.v_pool = _to_dev(relayout(v_pool), device)
         self.k_scale = None if k_scale is None else _to_dev(np.asarray(k_scale, np.float32), device)
         self.v_scale = None if v_scale is None else _to_dev(np.asarray(v_scale, np.float32), device)
         self.routes = _to_dev(np.asarray(routes, np.int32).reshape(-1, 6), device)
@@ -49,7 +55,7 @@ class DecodeState:
         B, Hq, D = self.q.shape
         R = self.routes.shape[0]
         self.num_seqs = B
-        self.shape = kf.shape_of(self.q, self.k_pool, self.page_ids, scale)
+        self.shape = kf.shape_of(self.q, self.k_pool, self.page_ids, scale, self.kv_layout)
         self.workspace = kf.alloc_workspace(self.shape, R, self.max_pages_per_route, device)
         self.o_part = torch.empty((R, Hq, D), dtype=torch.float32, device=device)
         self.lse_part = torch.empty((R, Hq), dtype=torch.float32, device=device)
@@ -58,13 +64,14 @@ class DecodeState:
         self.err_flags = torch.zeros(1, dtype=torch.int32, device=device)
 
     @classmethod
-    def from_instance(cls, inst, device="cuda"):
+    def from_instance(cls, inst, device="cuda", kv_layout=None):
         """Upload a kf_workloads.Instance (duck-typed)."""
         return cls(q=inst.q, k_pool=inst.k_pool, v_pool=inst.v_pool, routes=inst.routes,
                    page_ids=inst.page_ids, seq_route_begin=inst.seq_route_begin,
                    tail_route=inst.tail_route, scale=inst.scale,
                    max_pages_per_route=inst.max_pages_per_route,
-                   k_scale=inst.k_scale, v_scale=inst.v_scale, device=device)
+                   k_scale=inst.k_scale, v_scale=inst.v_scale, device=device,
+                   kv_layout=kv_layout)
 
     def upload_new_tokens(self, k_new: np.ndarray, v_new: np.ndarray):
         return _to_dev(k_new, self.device), _to_dev(v_new, self.device)

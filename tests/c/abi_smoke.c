@@ -46,7 +46,8 @@ int main(void) {
     fails |= 256;
 
   /* launch plan of the Llama-3.1-8B layer (no GPU: 256 compute units assumed) */
-  const kf_shape llama = {16, 32, 8, KF_HEAD_DIM, KF_PAGE_SIZE, KF_KV_BF16, 33000, 33000, 0.0884f};
+  const kf_shape llama = {16, 32, 8, KF_HEAD_DIM, KF_PAGE_SIZE, KF_KV_BF16, 33000, 33000, 0.0884f,
+                          KF_KV_PAGE_MAJOR};
   int32_t chunk_pages = 0, max_chunks = 0, units_per_wg = 0;
   if (kf_partial_attn_plan(&llama, 64, 516, 0, &chunk_pages, &max_chunks, &units_per_wg) != KF_OK ||
       chunk_pages != 516 || max_chunks != 1 || units_per_wg != 2)

@@ -43,7 +43,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 def test_struct_layouts_match_header():
     assert ctypes.sizeof(kf.Route) == 24
-    assert ctypes.sizeof(kf.Shape) == 36
+    assert ctypes.sizeof(kf.Shape) == 40
     assert ctypes.sizeof(policy.Params) == 80
     assert policy.RANGE_DT.itemsize == 24 and policy.NODE_DT.itemsize == 32
     assert policy.EVENT_DT.itemsize == 24 and policy.ROUTE_DT.itemsize == 24
@@ -63,7 +63,7 @@ def _shape(**kw):
     d.update(kw)
     s = kf.make_shape(d["num_seqs"], d["num_q_heads"], d["num_kv_heads"], d["kv_dtype"],
                       d["num_pages"], d["num_page_ids"], d["scale"])
-    for k in ("head_dim", "page_size"):
+    for k in ("head_dim", "page_size", "kv_layout"):
         if k in kw:
             setattr(s, k, kw[k])
     return s
@@ -92,6 +92,8 @@ def _partial(lib, shape, **kw):
     ({"num_q_heads": 34, "num_kv_heads": 2}, {}, -2),  # group 17 > 16
     ({"kv_dtype": 1}, {}, -1),                       # fp8 without scales
     ({"kv_dtype": 5}, {}, -2),
+    ({"kv_layout": 2}, {}, -2),                      # unknown pool layout
+    ({"kv_layout": -1}, {}, -2),
     ({"num_pages": 0}, {}, -1),
     ({"scale": float("nan")}, {}, -1),
     ({}, dict(R=-1), -1),
