@@ -146,7 +146,9 @@ int kf_kv_append(const kf_shape* shape, void* k_pool, void* v_pool, float* k_sca
  * kf_partial_attn_subset over any part of it, and it covers ragged and
  * equal routes alike: it does not depend on shape->num_page_ids, so it stays
  * valid as the page table grows or shrinks.  No initialisation is needed;
- * contents are dead between calls.  Returns 0 for invalid arguments.
+ * contents are dead between calls.  Returns 0 for invalid arguments and for
+ * num_routes or num_kv_heads above 65535, which no launch accepts.  Host
+ * only; its time is bounded for any argument (well under a millisecond).
  */
 size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes,
                                        int32_t max_pages_per_route);

@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include <atomic>
+#include <initializer_list>
 
 #include "kf.h"
 #include "kf_internal.h"
@@ -61,26 +62,41 @@ int cu_count() {
 }
 }  // namespace
 
-ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_pages_per_route,
-                      int64_t num_page_ids, bool fp8) {
+bool ragged_table(int64_t num_page_ids, int32_t num_routes, int32_t max_pages_per_route) {
+  // The page table is under 90% of routes x max pages: the routes reserve
+  // different page counts.  reserved <= 2^62; ids * 10 < 2^35.
+  const int64_t reserved = (int64_t)(num_routes > 0 ? num_routes : 0) *
+                           (int64_t)(max_pages_per_route > 0 ? max_pages_per_route : 0);
+  if (reserved <= 0) return false;
+  const int64_t ids = num_page_ids > 0 ? num_page_ids : 0;
+  // ids * 10 < reserved * 9, without forming reserved * 9 where it would
+  // overflow (there ids * 10 < 2^35 is far below it)
+  return reserved > INT64_MAX / 16 ? true : ids * 10 < reserved * 9;
+}
+
+int64_t ranges_per_slot(bool fp8) { return fp8 ? 6 : 12; }
+
+namespace {
+// plan_chunks for a GPU with `slots` resident workgroups (two per CU).
+ChunkPlan plan_for_slots(int32_t num_routes, int32_t num_kv_heads, int32_t max_pages_per_route,
+                         bool ragged, bool fp8, int64_t slots) {
   const int64_t units = (int64_t)num_routes * num_kv_heads;
-  const int64_t slots = 2 * (int64_t)cu_count();  // resident workgroups at two per CU
   const int32_t whole = max_pages_per_route > 0 ? max_pages_per_route : 1;
   if (units <= 0 || max_pages_per_route <= kMinSplitPages) return {whole, 1};
-  // Ragged routes are recognised by a page table under 90% of routes x max
-  // pages (the routes' reservations sum to it).  Whole units suit equal
-  // lengths only: a ragged batch that fills whole rounds would wait for its
-  // longest unit, so it is cut into ranges like any other.
-  const bool ragged = num_page_ids * 10 < (int64_t)num_routes * max_pages_per_route * 9;
+  // Whole units suit equal lengths only: a ragged batch that fills whole
+  // rounds would wait for its longest unit, so it is cut into ranges like
+  // any other.
   if (units >= slots && units % slots == 0 && !ragged) return {whole, 1};
   // Fewer units than slots: units of equal length run best as about one
   // range per slot, one round of workgroups; ragged routes need more ranges
   // for the dispatcher to balance.  More units than slots: about 12 ranges
   // per slot, 6 for fp8 pools, whose pages hold half the bytes, so that a
-  // workgroup streams about as much either way.
-  const int64_t many = fp8 ? 6 : 12;
+  // workgroup streams about as much either way.  From `many` ranges per slot
+  // worth of units on, every unit is one range.
+  const int64_t many = ranges_per_slot(fp8);
+  if (units >= many * slots) return {whole, 1};
   const int64_t target = (units < slots ? (ragged ? 4 : 1) : many) * slots;
-  int64_t c = (units * max_pages_per_route + target - 1) / target;
+  int64_t c = (units * max_pages_per_route + target - 1) / target;  // < 2^31 * 2^15
   if (c < kMinSplitPages) c = kMinSplitPages;
   if (c >= max_pages_per_route) return {whole, 1};
   int64_t m = (max_pages_per_route + c - 1) / c;
@@ -94,8 +110,10 @@ ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_page
     if (c < kMinSplitPages) c = kMinSplitPages;
     m = (max_pages_per_route + c - 1) / c;
     // with many ranges the rounding can keep the count even: shorten the
-    // ranges until it is odd (or the 16-page floor is reached)
-    for (int64_t cc = c - 1; m % 2 == 0 && cc >= kMinSplitPages; --cc) {
+    // ranges until it is odd (or the 16-page floor is reached); a bounded
+    // search, so that planning stays O(1)
+    for (int64_t cc = c - 1, tries = 0; m % 2 == 0 && cc >= kMinSplitPages && tries < 64;
+         --cc, ++tries) {
       const int64_t mm = (max_pages_per_route + cc - 1) / cc;
       if (mm % 2 == 1) {
         c = cc;
@@ -108,6 +126,13 @@ ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_page
     c = (max_pages_per_route + m - 1) / m;
   }
   return {(int32_t)c, (int32_t)m};
+}
+}  // namespace
+
+ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_pages_per_route,
+                      bool ragged, bool fp8) {
+  return plan_for_slots(num_routes, num_kv_heads, max_pages_per_route, ragged, fp8,
+                        2 * (int64_t)cu_count());
 }
 
 // Unsplit bf16 launches over the whole table with at least two units per
@@ -162,6 +187,7 @@ const char* kf_version(void) { return "kf 0.1 gfx950"; }
 size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes,
                                        int32_t max_pages_per_route) {
   if (check_shape(shape) != KF_OK || num_routes < 0 || max_pages_per_route < 0) return 0;
+  if (num_routes > kf::kMaxLaunchRoutes || shape->num_kv_heads > kf::kMaxLaunchRoutes) return 0;
   const int32_t group = shape->num_q_heads / shape->num_kv_heads;
   const bool fp8 = shape->kv_dtype == KF_KV_FP8_E4M3;
   // The largest need of any launch of at most num_routes routes: fewer routes
@@ -169,11 +195,15 @@ size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes
   // a whole route table must also serve a launch over a subset of it.  Both
   // readings of the page table (ragged routes or not) are covered, so the
   // size does not depend on shape->num_page_ids, which grows with the table.
-  size_t most = 0;
-  for (int32_t m = num_routes > 0 ? 1 : 0; m <= num_routes; ++m) {
-    for (const int64_t pids : {(int64_t)0, INT64_MAX}) {
+  // Launches whose units reach ranges_per_slot * slots keep every unit whole
+  // and need no workspace, so at most that many route counts are visited.
+  const int64_t slots = 2 * (int64_t)kf::cu_count();
+  const int64_t split_units = kf::ranges_per_slot(fp8) * slots;
+  size_t most = 256;
+  for (int32_t m = 1; m <= num_routes && (int64_t)m * shape->num_kv_heads < split_units; ++m) {
+    for (const bool ragged : {false, true}) {
       const kf::ChunkPlan plan =
-          kf::plan_chunks(m, shape->num_kv_heads, max_pages_per_route, pids, fp8);
+          kf::plan_for_slots(m, shape->num_kv_heads, max_pages_per_route, ragged, fp8, slots);
       const size_t t = kf::workspace_layout(m, shape->num_kv_heads, group, plan.max_chunks).total;
       if (t > most) most = t;
     }
@@ -188,10 +218,11 @@ int kf_partial_attn_plan(const kf_shape* shape, int32_t num_launch, int32_t max_
   if (st != KF_OK) return st;
   if (num_launch < 0 || max_pages_per_route < 0 || (route_list_launch != 0 && route_list_launch != 1))
     return KF_ERR_INVALID_ARG;
-  if (num_launch > 65535 || shape->num_kv_heads > 65535) return KF_ERR_UNSUPPORTED;
-  const kf::ChunkPlan plan = kf::plan_chunks(num_launch, shape->num_kv_heads, max_pages_per_route,
-                                             shape->num_page_ids,
-                                             shape->kv_dtype == KF_KV_FP8_E4M3);
+  if (num_launch > kf::kMaxLaunchRoutes || shape->num_kv_heads > kf::kMaxLaunchRoutes) return KF_ERR_UNSUPPORTED;
+  const kf::ChunkPlan plan = kf::plan_chunks(
+      num_launch, shape->num_kv_heads, max_pages_per_route,
+      kf::ragged_table(shape->num_page_ids, num_launch, max_pages_per_route),
+      shape->kv_dtype == KF_KV_FP8_E4M3);
   if (chunk_pages) *chunk_pages = plan.chunk_pages;
   if (max_chunks) *max_chunks = plan.max_chunks;
   if (units_per_wg)
@@ -254,7 +285,7 @@ int prepare_partial(const kf_shape* shape, const void* q, const void* k_pool, co
   if (st != KF_OK) return st;
   if (num_routes < 0 || num_launch < 0 || max_pages_per_route < 0) return KF_ERR_INVALID_ARG;
   if (num_launch == 0) return KF_OK;
-  if (num_launch > 65535 || shape->num_kv_heads > 65535) return KF_ERR_UNSUPPORTED;
+  if (num_launch > kf::kMaxLaunchRoutes || shape->num_kv_heads > kf::kMaxLaunchRoutes) return KF_ERR_UNSUPPORTED;
   const bool fp8 = shape->kv_dtype == KF_KV_FP8_E4M3;
   if (!q || !k_pool || !v_pool || !routes || !o_part || !lse_part || !err_flags ||
       (shape->num_page_ids > 0 && !page_ids))
@@ -266,9 +297,10 @@ int prepare_partial(const kf_shape* shape, const void* q, const void* k_pool, co
   for (const void* p : p4)
     if (p && !aligned(p, 4)) return KF_ERR_INVALID_ARG;
   const int32_t group = shape->num_q_heads / shape->num_kv_heads;
-  const kf::ChunkPlan plan = kf::plan_chunks(num_launch, shape->num_kv_heads, max_pages_per_route,
-                                             shape->num_page_ids,
-                                             shape->kv_dtype == KF_KV_FP8_E4M3);
+  const kf::ChunkPlan plan = kf::plan_chunks(
+      num_launch, shape->num_kv_heads, max_pages_per_route,
+      kf::ragged_table(shape->num_page_ids, num_launch, max_pages_per_route),
+      shape->kv_dtype == KF_KV_FP8_E4M3);
   const kf::WorkspaceLayout l =
       kf::workspace_layout(num_launch, shape->num_kv_heads, group, plan.max_chunks);
   if (!workspace || !aligned(workspace, 256) || workspace_bytes < l.total) return KF_ERR_WORKSPACE;

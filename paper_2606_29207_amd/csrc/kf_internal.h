@@ -17,6 +17,7 @@ constexpr int kDim = KF_HEAD_DIM;     // head dimension
 constexpr int kWaves = 4;             // waves per unit (a workgroup, or half of one)
 constexpr int kMinSplitPages = 16;    // smallest page range a split workgroup gets
 constexpr int kMaxPagesTwoUnit = 2048;  // longest units run two per workgroup (bf16, unsplit)
+constexpr int kMaxLaunchRoutes = 65535;  // routes per launch and KV heads: grid dimension limits
 
 struct AppendArgs {
   void* k_pool;
@@ -98,8 +99,14 @@ struct WorkspaceLayout {
 struct ChunkPlan {
   int32_t chunk_pages, max_chunks;
 };
+// True when the page table holds under 90% of num_routes * max_pages_per_route
+// entries: the routes reserve different page counts (ragged lengths).
+bool ragged_table(int64_t num_page_ids, int32_t num_routes, int32_t max_pages_per_route);
+// Ranges per resident slot when units outnumber slots (12 bf16, 6 fp8); from
+// that many units per slot on, every unit runs whole.
+int64_t ranges_per_slot(bool fp8);
 ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_pages_per_route,
-                      int64_t num_page_ids, bool fp8);
+                      bool ragged, bool fp8);
 // Units per workgroup of a partial-attention launch of num_launch routes
 // (1 or 2); route_list: a launch over a route list (kf_partial_attn_subset).
 int32_t units_per_workgroup(bool fp8, bool route_list, const ChunkPlan& plan, int32_t num_launch,

@@ -200,11 +200,12 @@ def _workspace_need(units_routes, H, G, maxp, ragged, slots=512, fp8=False):
     if (units >= slots or ragged) and m % 2 == 0:
         c = max(-(-maxp // (m + 1)), 16)
         m = -(-maxp // c)
-        cc = c - 1
-        while m % 2 == 0 and cc >= 16:
+        cc, tries = c - 1, 0
+        while m % 2 == 0 and cc >= 16 and tries < 64:   # a bounded search
             if -(-maxp // cc) % 2 == 1:
                 c, m = cc, -(-maxp // cc)
             cc -= 1
+            tries += 1
     recs = units * m * G
     return rup(recs * 2 * 4) + rup(recs * 128 * 4)
 
@@ -234,6 +235,29 @@ def test_workspace_bytes(lib):
         assert kf.partial_attn_workspace_bytes(s, 48, 1024) == max(need(k, 1024) for k in range(49))
     assert kf.partial_attn_workspace_bytes(s, -1, 5) == 0
     assert kf.partial_attn_workspace_bytes(_shape(head_dim=64), 4, 5) == 0
+
+
+def test_workspace_query_is_bounded(lib):
+    """The query refuses what no launch accepts (above 65535 routes or KV
+    heads) and stays fast for any argument: only route counts whose units can
+    be split are visited."""
+    for H in (1, 2, 8, 65535, 65536):
+        for dt in (kf.KV_BF16, kf.KV_FP8_E4M3):
+            for R in (1, 6144, 65535, 65536, 2 ** 31 - 1):
+                for maxp in (0, 17, 1000, 2 ** 31 - 1):
+                    s = _shape(num_seqs=4, num_q_heads=H, num_kv_heads=H, kv_dtype=dt)
+                    best = min(_timed(lambda: kf.partial_attn_workspace_bytes(s, R, maxp))
+                               for _ in range(3))
+                    n = kf.partial_attn_workspace_bytes(s, R, maxp)
+                    assert (n == 0) == (R > 65535 or H > 65535), (H, dt, R, maxp, n)
+                    assert best < 1e-3, (H, dt, R, maxp, best)
+
+
+def _timed(fn):
+    import time
+    t = time.perf_counter()
+    fn()
+    return time.perf_counter() - t
 
 
 def test_partial_attn_plan(lib):
