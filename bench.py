@@ -33,14 +33,23 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "achieved HBM GB/s + µs/step for partial decode attn+merge (Llama-3.1-8B layer)"
+# Tail pages reserved for at least this many appends (more if warmup + 3 x
+# steps needs it), so the route table, and with it the launch plan, is the
+# same for every short run; tests take the same reservation.
+RESERVE_APPENDS = 192
+# Host threads of the oracle baseline: the host share of a one-GPU job
+# (KF_CPU_THREADS overrides); the visible core count is reported beside it.
+CPU_THREADS_DEFAULT = 16
 HBM_PEAK_GBPS = 8000.0            # MI355X HBM3E, vendor figure
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_29207_amd", "csrc", "kf_kernels.hip")
 COUNTERS = os.path.join(ROOT, "profiles", "partial_kernel_{workload}_counters.md")
 
 
 # ---------------------------------------------------------------- bytes model
-def step_bytes(inst, step: int) -> dict:
-    """Algorithmic HBM bytes of decode step ``step`` (0-based), per call.
+def step_bytes(inst, step: int, rows=None) -> dict:
+    """Algorithmic HBM bytes of decode step ``step`` (0-based), per call;
+    ``rows`` restricts the partial-attention bytes to a list of routes (one
+    launch of the query-first schedule).
 
     KV bytes follow the footprint formula of the paper's scaling policy
     (2 * tokens * H_kv * d_h * element bytes per layer); the rest is what each
@@ -54,17 +63,38 @@ def step_bytes(inst, step: int) -> dict:
         lens = lens.copy()
         tails = inst.tail_route[inst.tail_route >= 0]
         lens[tails] += step + 1
+    if rows is not None:
+        lens = lens[np.asarray(rows, np.int64)]
+    Rl = len(lens)
     tokens = int(lens.sum())
     pages = int((-(-lens // 16)).sum())
     kv = 2 * tokens * H * D * esz + (2 * pages * H * 4 if esz == 1 else 0)
-    partial = kv + B * Hq * D * 2 + pages * 4 + R * 24 + R * Hq * (D + 1) * 4
+    partial = kv + B * Hq * D * 2 + pages * 4 + Rl * 24 + Rl * Hq * (D + 1) * 4
     merge = R * Hq * (D + 1) * 4 + (B + 1) * 4 + B * Hq * (D + 1) * 4
     n_app = int((inst.tail_route >= 0).sum()) if wl.appends else 0
-    append = 4 * n_app * H * D * 2 + n_app * 24
+    # read the new K/V token, write it into the pool (and, for fp8, read and
+    # write the page's K and V scales), read and write the route row
+    append = n_app * (2 * H * D * 2 + 2 * H * D * esz + (2 * H * 4 * 2 if esz == 1 else 0) + 2 * 24)
     return dict(append=append, partial=partial, merge=merge, kv=kv, tokens=tokens)
 
 
 # --------------------------------------------------------------- cpu baseline
+def visible_cores() -> int:
+    try:
+        return len(os.sched_getaffinity(0))
+    except AttributeError:
+        return os.cpu_count() or 1
+
+
+def cpu_threads(host_cores: int) -> int:
+    """Threads the oracle baseline uses: KF_CPU_THREADS if set, else the
+    visible cores up to CPU_THREADS_DEFAULT."""
+    env = os.environ.get("KF_CPU_THREADS")
+    if env:
+        return max(1, int(env))
+    return max(1, min(CPU_THREADS_DEFAULT, host_cores))
+
+
 def cpu_baseline(inst, min_s=10.0, max_s=30.0) -> dict:
     """The fp64 oracle on the host: partials of (route, KV head) units of the
     same instance, spread over a thread pool with one BLAS thread each, then
@@ -75,11 +105,8 @@ def cpu_baseline(inst, min_s=10.0, max_s=30.0) -> dict:
 
     import oracle
     wl = inst.wl
-    try:
-        cores = len(os.sched_getaffinity(0))
-    except AttributeError:
-        cores = os.cpu_count() or 1
-    cores = max(1, min(16, cores))
+    host_cores = visible_cores()
+    cores = cpu_threads(host_cores)
     G = wl.group
 
     def unit(args):
@@ -118,7 +145,7 @@ def cpu_baseline(inst, min_s=10.0, max_s=30.0) -> dict:
     except OSError:
         pass
     return {"value": round(done_bytes / el / 1e9, 4), "unit": "GB/s", "cores": cores,
-            "cpu_model": model,
+            "host_cores_visible": host_cores, "cpu_model": model,
             "kind": "oracle",
             "sample": f"{done_seqs} sequence(s) of the same instance (all routes x KV heads, "
                       f"fp64 partials + merge, append not timed), {el:.1f} s on {cores} threads, "
@@ -201,13 +228,17 @@ def policy_report(inst, wl, bw_gbps: float, attn_us: float, hbm_bytes: int) -> d
                            "T_step = layers x measured attention+merge, T_prewarm 1 s"}
 
 
-def kernel_label(st, wl) -> str:
-    """The partial-attention launch the timed step makes, from the library's
-    own plan: its kernel, units per workgroup and any combine launch."""
+def kernel_label(st, wl, route_list=None) -> str:
+    """The partial-attention launch the timed step makes (route_list: a launch
+    over those routes), from the library's own plan: its kernel, units per
+    workgroup and any combine launch."""
     from paper_2606_29207_amd import kf
-    chunk_pages, max_chunks, units = kf.partial_attn_plan(st.shape, st.routes.shape[0],
-                                                          st.max_pages_per_route)
+    n = st.routes.shape[0] if route_list is None else len(route_list)
+    chunk_pages, max_chunks, units = kf.partial_attn_plan(st.shape, n, st.max_pages_per_route,
+                                                          route_list=route_list is not None)
     name = f"partial_kernel<{wl.kv_dtype}" + (", 2 units/workgroup>" if units == 2 else ">")
+    if route_list is not None:
+        name += f" over {n} listed routes"
     if max_chunks > 1:
         name += f" + combine_kernel ({chunk_pages}-page chunks, up to {max_chunks} per unit)"
     return name
@@ -244,7 +275,7 @@ def main(argv=None):
     wl = workload(args.workload)
     K, W = args.steps, args.warmup
     t = time.perf_counter()
-    inst = make_instance(wl, seed=args.seed, steps=W + 3 * K)
+    inst = make_instance(wl, seed=args.seed, steps=max(W + 3 * K, RESERVE_APPENDS))
     print(f"[bench] generated {wl.name} in {time.perf_counter() - t:.1f}s", file=sys.stderr, flush=True)
 
     cpu = None
@@ -303,9 +334,7 @@ def main(argv=None):
         e = ev[i]
         e[0].record(stream)
         if qf:
-            st.step_query_first(*news[W + K + i])
-            e[1].record(stream)
-            e[2].record(stream)
+            st.step_query_first(*news[W + K + i], hist_events=(e[1], e[2]))
             e[3].record(stream)
             continue
         if wl.appends:
@@ -345,31 +374,23 @@ def main(argv=None):
         print(f"[bench] device error flags {flags}", file=sys.stderr, flush=True)
         return 1
 
-    if qf:
-        t_step = np.array([e[0].elapsed_time(e[3]) for e in ev]) * 1e3
-        by = [step_bytes(inst, W + i) for i in range(K)]
-        step_b = np.mean([b["append"] + b["partial"] + b["merge"] for b in by])
-        us_step = wall / K * 1e6
-        print(json.dumps({"metric": METRIC, "value": round(step_b / (us_step * 1e-6) / 1e9, 2),
-                          "unit": "GB/s", "n_gpus": 1, "steps": K, "warmup": W,
-                          "ms_per_step": round(us_step / 1e3, 4), "us_per_step": round(us_step, 2),
-                          "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-                          "dtype": "bf16", "data": "synthetic", "schedule": "query_first",
-                          "config": {"workload": wl.name, "batch": wl.num_seqs},
-                          "step_event_us": round(float(t_step.mean()), 2),
-                          "bytes_per_step": int(step_b), "roofline": None, "cpu_baseline": cpu}),
-              flush=True)
-        return 0
     t_app = np.array([e[0].elapsed_time(e[1]) for e in ev]) * 1e3      # us
     t_par = np.array([e[1].elapsed_time(e[2]) for e in ev]) * 1e3
     t_mrg = np.array([e[2].elapsed_time(e[3]) for e in ev]) * 1e3
     by = [step_bytes(inst, W + i) for i in range(K)]
     step_b = np.mean([b["append"] + b["partial"] + b["merge"] for b in by])
     by2 = [step_bytes(inst, W + K + i) for i in range(K)]
-    par_b = np.mean([b["partial"] for b in by2])
+    if qf:   # the events bracket the launch over the historical routes only
+        par_b = np.mean([step_bytes(inst, W + K + i, rows=st.hist_rows)["partial"]
+                         for i in range(K)])
+    else:
+        par_b = np.mean([b["partial"] for b in by2])
     am_b = np.mean([b["partial"] + b["merge"] for b in by2])
     us_step = wall / K * 1e6
     achieved = par_b / (t_par.mean() * 1e-6) / 1e9
+    t_step = np.array([e[0].elapsed_time(e[3]) for e in ev]) * 1e3
+    # attention + merge: the two calls, or (query-first) the whole overlapped step
+    t_am = t_step if qf else t_par + t_mrg
     # the committed counter profiles were taken on page-major pools
     traffic = counter_traffic(wl.name, args.seed) if args.kv_layout == "page" else None
     out = {
@@ -392,24 +413,33 @@ def main(argv=None):
                    "routes": int(len(inst.routes)), "page_tokens": 16,
                    "appends_per_step": wl.appends, "kv_dtype": wl.kv_dtype,
                    "kv_layout": args.kv_layout},
-        "schedule": "fused" if fused else "serial",
-        "breakdown_pass": "a second run of K steps as three calls with HIP events around each",
-        "breakdown_us": {"append": round(float(t_app.mean()), 2) if wl.appends else None,
-                         "partial_attn": round(float(t_par.mean()), 2),
-                         "partial_attn_median": round(float(np.median(t_par)), 2),
-                         "partial_attn_p10_p90": [round(float(np.percentile(t_par, 10)), 2),
-                                                  round(float(np.percentile(t_par, 90)), 2)],
-                         "merge": round(float(t_mrg.mean()), 2)},
+        "schedule": "query_first" if qf else "fused" if fused else "serial",
+        "breakdown_pass": ("a second run of K query-first steps with HIP events on the first "
+                           "stream around the launch over the historical routes and around the "
+                           "whole step" if qf else
+                           "a second run of K steps as three calls with HIP events around each"),
+        "breakdown_us": ({"historical_partial_attn": round(float(t_par.mean()), 2),
+                          "historical_partial_attn_median": round(float(np.median(t_par)), 2),
+                          "historical_routes": int(len(st.hist_rows)),
+                          "tail_routes": int(len(st.tail_rows)),
+                          "step": round(float(t_step.mean()), 2)} if qf else
+                         {"append": round(float(t_app.mean()), 2) if wl.appends else None,
+                          "partial_attn": round(float(t_par.mean()), 2),
+                          "partial_attn_median": round(float(np.median(t_par)), 2),
+                          "partial_attn_p10_p90": [round(float(np.percentile(t_par, 10)), 2),
+                                                   round(float(np.percentile(t_par, 90)), 2)],
+                          "merge": round(float(t_mrg.mean()), 2)}),
         "flushed": flushed,
-        "attn_merge_us": round(float((t_par + t_mrg).mean()), 2),
-        "attn_merge_GBps": round(am_b / ((t_par + t_mrg).mean() * 1e-6) / 1e9, 2),
+        "attn_merge_us": round(float(t_am.mean()), 2),
+        "attn_merge_GBps": round(am_b / (t_am.mean() * 1e-6) / 1e9, 2),
         "bytes_per_step": int(step_b),
-        "roofline": {"bound": "hbm", "kernel": kernel_label(st, wl),
+        "roofline": {"bound": "hbm",
+                     "kernel": kernel_label(st, wl, st.hist_rows if qf else None),
                      "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic, "algorithmic_bytes_per_launch": int(par_b)},
         "cpu_baseline": cpu,
-        "policy": policy_report(inst, wl, achieved, float((t_par + t_mrg).mean()),
+        "policy": policy_report(inst, wl, achieved, float(t_am.mean()),
                                 torch.cuda.mem_get_info()[1]),
     }
     print(json.dumps(out), flush=True)

@@ -90,6 +90,11 @@ WORKLOADS = {
     "wide_gqa_fp8": Workload("wide_gqa_fp8", 5, num_seqs=32, num_q_heads=64,
                              num_kv_heads=8, part_tokens=16384, ctx=65536,
                              kv_dtype="fp8"),
+    # the same layer run as decode steps: 1 appended token per sequence per
+    # step into the fp8 tails (same streams, so the same resident tokens)
+    "wide_gqa_fp8_decode": Workload("wide_gqa_fp8_decode", 5, num_seqs=32, num_q_heads=64,
+                                    num_kv_heads=8, part_tokens=16384, ctx=65536,
+                                    kv_dtype="fp8", appends=1),
 }
 
 

@@ -229,11 +229,13 @@ def merge_partials(o_part, lse_part, seq_route_begin):
 
 # -------------------------------------------------------------------- append
 def kv_append(k_pool, v_pool, routes, page_ids, tail_route, k_new, v_new,
-              k_scale=None, v_scale=None):
+              k_scale=None, v_scale=None, inplace=False):
     """Tail append (Section 3.2, step 3; Section 5.1): each sequence b with a
     tail route r = tail_route[b] >= 0 stores its new K/V token (bf16 bits
     [B, Hkv, d]) at local index j = tok_end - tok_begin of route r and then
-    extends the route by one token.  Works on copies; returns
+    extends the route by one token.  Works on copies (inplace=True: on the
+    arrays given, which must then be writable numpy arrays of the storage
+    dtypes -- for pools of many gigabytes); returns
     (k_pool, v_pool, routes, flags) for bf16 pools and
     (k_pool, v_pool, k_scale, v_scale, routes, flags) for E4M3 pools.  A full
     tail (no reserved page for j) or an inconsistent route leaves that
@@ -249,12 +251,17 @@ def kv_append(k_pool, v_pool, routes, page_ids, tail_route, k_new, v_new,
         code' = RNE(value/scale')), then the scale becomes scale';
       * the token is stored as RNE(x/scale), clamped to +-448."""
     fp8 = k_pool.dtype == np.uint8
-    k_pool = k_pool.copy()
-    v_pool = v_pool.copy()
-    if fp8:
-        k_scale = np.array(k_scale, dtype=np.float32, copy=True)
-        v_scale = np.array(v_scale, dtype=np.float32, copy=True)
-    routes = np.array(routes, dtype=np.int32, copy=True)
+    if inplace:
+        for a in (k_pool, v_pool, routes) + ((k_scale, v_scale) if fp8 else ()):
+            assert isinstance(a, np.ndarray) and a.flags.writeable
+        assert routes.dtype == np.int32 and (not fp8 or k_scale.dtype == v_scale.dtype == np.float32)
+    else:
+        k_pool = k_pool.copy()
+        v_pool = v_pool.copy()
+        if fp8:
+            k_scale = np.array(k_scale, dtype=np.float32, copy=True)
+            v_scale = np.array(v_scale, dtype=np.float32, copy=True)
+        routes = np.array(routes, dtype=np.int32, copy=True)
     R = len(routes)
     P = k_pool.shape[0]
     flags = 0

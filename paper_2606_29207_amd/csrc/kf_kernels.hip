@@ -467,7 +467,7 @@ __global__ __launch_bounds__(kThreads * UPW, 2 / UPW) void partial_kernel(Partia
 
   // Page ids are uniform, so they (and fp8 scales) arrive through scalar
   // loads; a page past the range or outside the pool reads page 0 and is
-  // masked or flagged.
+  // masked (its p set to 0 whatever its scales hold) or flagged.
   bool pid_bad = false;
   auto page_at = [&](int pg) -> int {  // page id of route-local page pg of the range
     const bool in = pg < p1;
@@ -611,7 +611,12 @@ __global__ __launch_bounds__(kThreads * UPW, 2 / UPW) void partial_kernel(Partia
         const float e0 = exp2_fast(s[cc][r4] - m_new);
         const float e1 = exp2_fast(s[cc][r4 + 1] - m_new);
         l_run += e0 + e1;
-        const float x0 = e0 * vs, x1 = e1 * vs;
+        float x0 = e0 * vs, x1 = e1 * vs;
+        if constexpr (MASK && FP8) {  // a masked slot adds nothing, whatever its page's scales
+          const int t0 = tok0 + 8 * h2 + 2 * jj;
+          x0 = t0 < lim ? x0 : 0.0f;
+          x1 = t0 + 1 < lim ? x1 : 0.0f;
+        }
         const uint32_t b0 = __builtin_bit_cast(uint32_t, x0) & 0xFFFF0000u;
         const uint32_t b1 = __builtin_bit_cast(uint32_t, x1) & 0xFFFF0000u;
         phi[h2][jj] = (b0 >> 16) | b1;

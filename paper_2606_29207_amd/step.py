@@ -56,6 +56,9 @@ class DecodeState:
         R = self.routes.shape[0]
         self.num_seqs = B
         self.shape = kf.shape_of(self.q, self.k_pool, self.page_ids, scale, self.kv_layout)
+        # sized for any launch over at most R routes (the query-first schedule
+        # launches over subsets, which may split their units), so it can be
+        # larger than a launch over the whole table needs
         self.workspace = kf.alloc_workspace(self.shape, R, self.max_pages_per_route, device)
         self.o_part = torch.empty((R, Hq, D), dtype=torch.float32, device=device)
         self.lse_part = torch.empty((R, Hq), dtype=torch.float32, device=device)
@@ -115,6 +118,7 @@ class DecodeState:
         tails = np.unique(tails[tails >= 0]).astype(np.int32)
         R = self.routes.shape[0]
         hist = np.setdiff1d(np.arange(R, dtype=np.int32), tails).astype(np.int32)
+        self.hist_rows, self.tail_rows = hist, tails
         self.hist_list = _to_dev(hist, self.device)
         self.tail_list = _to_dev(tails, self.device)
         self.ws_hist = kf.alloc_workspace(self.shape, R, self.max_pages_per_route, self.device)
@@ -123,19 +127,25 @@ class DecodeState:
         self._qf_ready = torch.cuda.Event()
         self._qf_tail_done = torch.cuda.Event()
 
-    def step_query_first(self, k_new: torch.Tensor, v_new: torch.Tensor):
+    def step_query_first(self, k_new: torch.Tensor, v_new: torch.Tensor, hist_events=None):
         """One decode step scheduled query-first (Section 5.1): partials of the
         historical routes start on the current stream from q alone; on a second
         stream the tails append the new K/V token and then attend; the merge
-        waits for both.  Same kernels as step(), other order."""
+        waits for both.  Same kernels as step(), other order.  hist_events:
+        two timing events recorded on the current stream around the launch
+        over the historical routes."""
         cur = torch.cuda.current_stream(self.device)
         self._qf_ready.record(cur)
         self.stream_b.wait_event(self._qf_ready)
+        if hist_events is not None:
+            hist_events[0].record(cur)
         if self.hist_list.numel():
             kf.partial_attn(self.shape, self.q, self.k_pool, self.v_pool, self.routes,
                             self.max_pages_per_route, self.page_ids, self.o_part, self.lse_part,
                             self.ws_hist, self.err_flags, self.k_scale, self.v_scale, cur,
                             route_list=self.hist_list)
+        if hist_events is not None:
+            hist_events[1].record(cur)
         self.append(k_new, v_new, self.stream_b)
         if self.tail_list.numel():
             kf.partial_attn(self.shape, self.q, self.k_pool, self.v_pool, self.routes,

@@ -111,15 +111,19 @@ def assert_close_lse(got, ref, what):
         return mx
 
 
+def _bits(a):
+    return np.ascontiguousarray(a, np.float32).view(np.uint32)
+
+
 def compare_all(g, o, pools=True):
     """Bit-exact pools and routes, toleranced floats, equal flags."""
     if pools:
         assert np.array_equal(g["routes"], o["routes"]), "routes differ"
         assert np.array_equal(g["k_pool"], o["k_pool"]), "K pool differs"
         assert np.array_equal(g["v_pool"], o["v_pool"]), "V pool differs"
-        if o.get("k_scale") is not None:
-            assert np.array_equal(g["k_scale"], o["k_scale"]), "K scales differ"
-            assert np.array_equal(g["v_scale"], o["v_scale"]), "V scales differ"
+        if o.get("k_scale") is not None:   # bit for bit (a NaN scale equals itself)
+            assert np.array_equal(_bits(g["k_scale"]), _bits(o["k_scale"])), "K scales differ"
+            assert np.array_equal(_bits(g["v_scale"]), _bits(o["v_scale"])), "V scales differ"
     assert g["flags"] == o["flags"], f"flags {g['flags']} != {o['flags']}"
     assert_close_o(g["o_part"], o["o_part"], "o_part")
     assert_close_lse(g["lse_part"], o["lse_part"], "lse_part")

@@ -77,10 +77,17 @@ def test_fp8_second_seed(gpu):
     compare_all(host(run_gpu(inst, 1)), run_oracle(inst, 1))
 
 
-def test_fp8_append_reencodes_pages_begun_by_appends():
+@pytest.mark.parametrize("fused", [False, True])
+def test_fp8_append_reencodes_pages_begun_by_appends(gpu, fused):
     """E4M3 append with one step's tokens 100x larger than the rest: pages
     begun by earlier appends of that step's tails are re-encoded to the new
-    scale; codes and scales bit-exact, attention within tolerance."""
+    scale; codes and scales bit-exact, attention within tolerance.
+
+    Bars: rel-L2 <= 1e-3 (o_part, out) and max|d| <= 1e-4 (lse_part, lse) as
+    everywhere.  The max|d| <= 2e-3 bar of o is stated for outputs of unit
+    scale; float32 error is relative, and the 100x tokens make outputs up to
+    ~400, so here it is 2e-3 * max(1, max|ref|) (measured: 2.9e-3 at
+    max|ref| 394, i.e. 7.5e-6 relative; rel-L2 4.9e-6; LSE 1.3e-5)."""
     wl = workload("wide_gqa_fp8", num_seqs=3, part_tokens=1024, appends=1)
     inst = make_instance(wl, seed=5, steps=24, seq_lens=[3000, 2048, 1111])
 
@@ -92,21 +99,19 @@ def test_fp8_append_reencodes_pages_begun_by_appends():
         return up(kn), up(vn)
 
     o = run_oracle(inst, steps=24, new_tokens=tokens)
-    g = host(run_gpu(inst, steps=24, new_tokens=tokens))
+    g = host(run_gpu(inst, steps=24, new_tokens=tokens, fused=fused))
     for key in ("routes", "k_pool", "v_pool", "k_scale", "v_scale"):
         assert np.array_equal(g[key], o[key]), f"{key} differs"
     assert g["flags"] == o["flags"] == 0
-    # the inputs are scaled up 100x, so the float32 error budget is too
     for key in ("o_part", "out"):
-        ref = o[key][np.isfinite(o[key])]
-        tol = 2e-3 * max(1.0, float(np.abs(ref).max()))
         assert np.array_equal(np.isnan(g[key]), np.isnan(o[key]))
-        assert float(np.abs(g[key] - o[key])[np.isfinite(o[key])].max()) <= tol, key
-    for key in ("lse_part", "lse"):
         fin = np.isfinite(o[key])
-        assert np.array_equal(fin, np.isfinite(g[key]))
-        tol = 1e-4 * max(1.0, float(np.abs(o[key][fin]).max()))
-        assert float(np.abs(g[key] - o[key])[fin].max()) <= tol, key
+        d = (g[key] - o[key])[fin]
+        ref = o[key][fin]
+        assert float(np.abs(d).max()) <= 2e-3 * max(1.0, float(np.abs(ref).max())), key
+        assert float(np.linalg.norm(d) / np.linalg.norm(ref)) <= 1e-3, key
+    assert_close_lse(g["lse_part"], o["lse_part"], "lse_part")
+    assert_close_lse(g["lse"], o["lse"], "lse")
 
 
 def test_empty_tail_route_then_append(gpu):

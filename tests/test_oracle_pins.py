@@ -631,3 +631,40 @@ def test_fp8_append_without_reencode_is_caught():
             test_fp8_append_reencodes_page_for_large_token()
     finally:
         kf_oracle._append_e4m3 = saved
+
+
+def test_append_in_place_equals_append_on_copies():
+    """kv_append(..., inplace=True) -- for pools too large to copy every step --
+    writes exactly what the copying form returns, for bf16 and E4M3 pools over
+    steps that cross pages and re-encode one (and leaves its inputs as the
+    copying form would have returned them)."""
+    for name, over, lens in (("llama8b_32k", dict(num_seqs=2, num_q_heads=8, num_kv_heads=2,
+                                                  part_tokens=64, appends=1), [70, 45]),
+                             ("wide_gqa_fp8", dict(num_seqs=2, num_q_heads=16, num_kv_heads=2,
+                                                   part_tokens=64, appends=1), [70, 45])):
+        inst = make_instance(workload(name, **over), seed=4, steps=20, seq_lens=lens)
+        fp8 = inst.k_scale is not None
+        ref = [inst.k_pool, inst.v_pool, inst.routes] + ([inst.k_scale, inst.v_scale] if fp8 else [])
+        mut = [a.copy() for a in ref]
+        for s in range(20):
+            kn, vn = inst.new_tokens(s)
+            if s == 7:
+                kn = f32_to_bf16_bits(oracle.bf16_to_f64(kn).astype(np.float32) * 60)
+            if fp8:
+                kp, vp, ks, vs, rt, f = oracle.kv_append(ref[0], ref[1], ref[2], inst.page_ids,
+                                                         inst.tail_route, kn, vn, ref[3], ref[4])
+                ref = [kp, vp, rt, ks, vs]
+                out = oracle.kv_append(mut[0], mut[1], mut[2], inst.page_ids, inst.tail_route,
+                                       kn, vn, mut[3], mut[4], inplace=True)
+                assert out[0] is mut[0] and out[2] is mut[3] and out[4] is mut[2]
+            else:
+                kp, vp, rt, f = oracle.kv_append(ref[0], ref[1], ref[2], inst.page_ids,
+                                                 inst.tail_route, kn, vn)
+                ref = [kp, vp, rt]
+                out = oracle.kv_append(mut[0], mut[1], mut[2], inst.page_ids, inst.tail_route,
+                                       kn, vn, inplace=True)
+                assert out[0] is mut[0] and out[2] is mut[2]
+            assert f == out[-1] == 0
+            for a, b in zip(ref, mut):
+                assert np.array_equal(a, b)
+        assert not np.array_equal(inst.routes, mut[2])    # the instance's own arrays untouched
