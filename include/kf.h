@@ -99,8 +99,12 @@ enum {
   KF_ERR_HIP = -4,         /* the HIP runtime refused a launch */
   KF_ERR_CAPACITY = -5,    /* a caller-sized host output array is too small */
   KF_ERR_INFEASIBLE = -6,  /* no budget satisfies the constraints */
-  KF_ERR_HOST_MEMORY = -7  /* host-side temporaries could not be allocated */
+  KF_ERR_HOST_MEMORY = -7, /* host-side temporaries could not be allocated */
+  KF_ERR_SCRATCH_LIMIT = -8 /* the launch needs more than KF_SCRATCH_BYTES of scratch */
 };
+
+/* Size of the library's per-device scratch array (kf_decode_step_no_alloc). */
+#define KF_SCRATCH_BYTES ((size_t)32 << 20)
 
 enum { KF_KV_BF16 = 0, KF_KV_FP8_E4M3 = 1 };
 
@@ -260,6 +264,36 @@ int kf_decode_step(const kf_shape* shape, const void* q, void* k_pool, void* v_p
                    const int32_t* seq_route_begin, float* o_part, float* lse_part, float* out,
                    float* lse_out, void* workspace, size_t workspace_bytes, int32_t* err_flags,
                    void* stream);
+
+/*
+ * kf_decode_step_no_alloc -- kf_decode_step for callers that cannot allocate
+ * device memory or pass a workspace: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc.  Same arguments, results,
+ * flags and route updates as kf_decode_step, without workspace and
+ * workspace_bytes: the chunk partials of a split launch go through a scratch
+ * array of KF_SCRATCH_BYTES that the library holds in each device's memory
+ * from the first kernel launch on that device until the process ends.
+ * Allocates nothing and calls no allocating routine.  The first call on a
+ * device also looks up that device's array address (hipGetSymbolAddress, on
+ * the current device, which must be the stream's); make one call before
+ * capturing a graph of it.
+ * Returns KF_ERR_SCRATCH_LIMIT, before anything is launched, when the launch
+ * would need more scratch than KF_SCRATCH_BYTES: the size kf_partial_attn
+ * would require of its workspace for these routes (with 256 compute units,
+ * about 4 MiB per query head of a KV group when the (route, KV head) units
+ * outnumber two per compute unit without filling whole rounds; launches
+ * whose units are not split need none).
+ * All calls on one device share its array and nothing in it needs to start
+ * at zero; calls that may overlap on one device (streams not ordered with
+ * respect to each other) race on it and must be serialised by the caller.
+ */
+int kf_decode_step_no_alloc(const kf_shape* shape, const void* q, void* k_pool, void* v_pool,
+                            float* k_scale, float* v_scale, const void* k_new,
+                            const void* v_new, kf_route* routes, int32_t num_routes,
+                            const int32_t* tail_route, int32_t max_pages_per_route,
+                            const int32_t* page_ids, const int32_t* seq_route_begin,
+                            float* o_part, float* lse_part, float* out, float* lse_out,
+                            int32_t* err_flags, void* stream);
 
 /*
  * kf_debug_gather -- test export: the resident tokens of route `route`

@@ -178,6 +178,7 @@ const char* kf_status_str(int status) {
     case KF_ERR_CAPACITY: return "output array too small";
     case KF_ERR_INFEASIBLE: return "infeasible budget";
     case KF_ERR_HOST_MEMORY: return "host memory exhausted";
+    case KF_ERR_SCRATCH_LIMIT: return "launch needs more than KF_SCRATCH_BYTES of scratch";
     default: return "unknown status";
   }
 }
@@ -380,6 +381,70 @@ int prepare_merge(int32_t num_seqs, int32_t num_routes, int32_t num_q_heads, int
   return KF_OK;
 }
 
+// The decode step of kf_decode_step (workspace given) and
+// kf_decode_step_no_alloc (use_scratch: the device's scratch array instead).
+int decode_step_impl(const kf_shape* shape, const void* q, void* k_pool, void* v_pool,
+                     float* k_scale, float* v_scale, const void* k_new, const void* v_new,
+                     kf_route* routes, int32_t num_routes, const int32_t* tail_route,
+                     int32_t max_pages_per_route, const int32_t* page_ids,
+                     const int32_t* seq_route_begin, float* o_part, float* lse_part, float* out,
+                     float* lse_out, void* workspace, size_t workspace_bytes, bool use_scratch,
+                     int32_t* err_flags, void* stream) {
+  kf::AppendArgs ap{};
+  kf::PartialArgs pa{};
+  kf::MergeArgs ma{};
+  int st = prepare_append(shape, k_pool, v_pool, k_scale, v_scale, k_new, v_new, routes,
+                          num_routes, tail_route, page_ids, err_flags, ap);
+  if (st != KF_OK) return st;
+  // The scratch array's size is checked like a workspace's, against a
+  // stand-in base address; the array's own address is taken only once every
+  // host check has passed.
+  char* const kStandIn = reinterpret_cast<char*>((uintptr_t)256);
+  if (use_scratch) {
+    workspace = kStandIn;
+    workspace_bytes = KF_SCRATCH_BYTES;
+  }
+  st = prepare_partial(shape, q, k_pool, v_pool, k_scale, v_scale, routes, num_routes, nullptr,
+                       num_routes, max_pages_per_route, page_ids, o_part, lse_part, workspace,
+                       workspace_bytes, err_flags, pa);
+  // the workspace is the last check of prepare_partial: a scratch array too
+  // small for this launch is reported after every argument check has passed
+  const bool over_scratch = use_scratch && st == KF_ERR_WORKSPACE;
+  if (st != KF_OK && !over_scratch) return st;
+  st = prepare_merge(shape->num_seqs, num_routes, shape->num_q_heads, shape->head_dim, o_part,
+                     lse_part, seq_route_begin, out, lse_out, err_flags, ma);
+  if (st != KF_OK) return st;
+  if (over_scratch) return KF_ERR_SCRATCH_LIMIT;
+  if (shape->num_seqs == 0) return KF_OK;
+  if (use_scratch && num_routes > 0) {
+    void* base = nullptr;
+    if (kf::scratch_address(&base) != hipSuccess) return KF_ERR_HIP;
+    const uintptr_t b = reinterpret_cast<uintptr_t>(base), s0 = reinterpret_cast<uintptr_t>(kStandIn);
+    pa.ws_ml = reinterpret_cast<float*>(b + (reinterpret_cast<uintptr_t>(pa.ws_ml) - s0));
+    pa.ws_o = reinterpret_cast<float*>(b + (reinterpret_cast<uintptr_t>(pa.ws_o) - s0));
+  }
+  const hipStream_t s = as_stream(stream);
+  const bool fp8 = shape->kv_dtype == KF_KV_FP8_E4M3;
+  if (num_routes == 0) {  // nothing to attend: the append kernel raises the flags
+    if (kf::launch_append(ap, fp8, s) != hipSuccess) return KF_ERR_HIP;
+    return kf::launch_merge(ma, s) == hipSuccess ? KF_OK : KF_ERR_HIP;
+  }
+  pa.k_new = ap.k_new;
+  pa.v_new = ap.v_new;
+  pa.tail_route = tail_route;
+  pa.k_pool_w = k_pool;
+  pa.v_pool_w = v_pool;
+  pa.k_scale_w = k_scale;
+  pa.v_scale_w = v_scale;
+  ma.routes = routes;
+  ma.tail_route = tail_route;
+  ma.page_ids = page_ids;
+  ma.num_pages = shape->num_pages;
+  ma.num_page_ids = shape->num_page_ids;
+  if (kf::launch_partial(pa, fp8, s) != hipSuccess) return KF_ERR_HIP;
+  return kf::launch_merge(ma, s) == hipSuccess ? KF_OK : KF_ERR_HIP;
+}
+
 }  // namespace
 
 extern "C" {
@@ -472,39 +537,22 @@ int kf_decode_step(const kf_shape* shape, const void* q, void* k_pool, void* v_p
                    const int32_t* seq_route_begin, float* o_part, float* lse_part, float* out,
                    float* lse_out, void* workspace, size_t workspace_bytes, int32_t* err_flags,
                    void* stream) {
-  kf::AppendArgs ap{};
-  kf::PartialArgs pa{};
-  kf::MergeArgs ma{};
-  int st = prepare_append(shape, k_pool, v_pool, k_scale, v_scale, k_new, v_new, routes,
-                          num_routes, tail_route, page_ids, err_flags, ap);
-  if (st != KF_OK) return st;
-  st = prepare_partial(shape, q, k_pool, v_pool, k_scale, v_scale, routes, num_routes, nullptr,
-                       num_routes, max_pages_per_route, page_ids, o_part, lse_part, workspace,
-                       workspace_bytes, err_flags, pa);
-  if (st != KF_OK) return st;
-  st = prepare_merge(shape->num_seqs, num_routes, shape->num_q_heads, shape->head_dim, o_part,
-                     lse_part, seq_route_begin, out, lse_out, err_flags, ma);
-  if (st != KF_OK || shape->num_seqs == 0) return st;
-  const hipStream_t s = as_stream(stream);
-  const bool fp8 = shape->kv_dtype == KF_KV_FP8_E4M3;
-  if (num_routes == 0) {  // nothing to attend: the append kernel raises the flags
-    if (kf::launch_append(ap, fp8, s) != hipSuccess) return KF_ERR_HIP;
-    return kf::launch_merge(ma, s) == hipSuccess ? KF_OK : KF_ERR_HIP;
-  }
-  pa.k_new = ap.k_new;
-  pa.v_new = ap.v_new;
-  pa.tail_route = tail_route;
-  pa.k_pool_w = k_pool;
-  pa.v_pool_w = v_pool;
-  pa.k_scale_w = k_scale;
-  pa.v_scale_w = v_scale;
-  ma.routes = routes;
-  ma.tail_route = tail_route;
-  ma.page_ids = page_ids;
-  ma.num_pages = shape->num_pages;
-  ma.num_page_ids = shape->num_page_ids;
-  if (kf::launch_partial(pa, fp8, s) != hipSuccess) return KF_ERR_HIP;
-  return kf::launch_merge(ma, s) == hipSuccess ? KF_OK : KF_ERR_HIP;
+  return decode_step_impl(shape, q, k_pool, v_pool, k_scale, v_scale, k_new, v_new, routes,
+                          num_routes, tail_route, max_pages_per_route, page_ids, seq_route_begin,
+                          o_part, lse_part, out, lse_out, workspace, workspace_bytes, false,
+                          err_flags, stream);
+}
+
+int kf_decode_step_no_alloc(const kf_shape* shape, const void* q, void* k_pool, void* v_pool,
+                            float* k_scale, float* v_scale, const void* k_new,
+                            const void* v_new, kf_route* routes, int32_t num_routes,
+                            const int32_t* tail_route, int32_t max_pages_per_route,
+                            const int32_t* page_ids, const int32_t* seq_route_begin,
+                            float* o_part, float* lse_part, float* out, float* lse_out,
+                            int32_t* err_flags, void* stream) {
+  return decode_step_impl(shape, q, k_pool, v_pool, k_scale, v_scale, k_new, v_new, routes,
+                          num_routes, tail_route, max_pages_per_route, page_ids, seq_route_begin,
+                          o_part, lse_part, out, lse_out, nullptr, 0, true, err_flags, stream);
 }
 
 }  // extern "C"

@@ -114,6 +114,10 @@ int32_t units_per_workgroup(bool fp8, bool route_list, const ChunkPlan& plan, in
 WorkspaceLayout workspace_layout(int32_t num_routes, int32_t num_kv_heads, int32_t group,
                                  int32_t max_chunks);
 
+// Address of the current device's scratch array (KF_SCRATCH_BYTES, for
+// kf_decode_step_no_alloc), looked up once per device.
+hipError_t scratch_address(void** out);
+
 hipError_t launch_append(const AppendArgs& a, bool fp8, hipStream_t stream);
 hipError_t launch_partial(const PartialArgs& a, bool fp8, hipStream_t stream);
 hipError_t launch_merge(const MergeArgs& a, hipStream_t stream);

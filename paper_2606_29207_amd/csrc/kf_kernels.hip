@@ -33,6 +33,8 @@
 // unit is chunked, the chunk partials go to the workspace and combine_kernel
 // (the next launch on the stream) merges them in chunk order, so results are
 // deterministic.
+#include <atomic>
+#include <mutex>
 #include <type_traits>
 
 #include "kf_internal.h"
@@ -943,6 +945,39 @@ hipError_t launch_partial_kernel(const PartialArgs& a, dim3 grid, hipStream_t st
 }
 
 }  // namespace
+
+// ------------------------------------------------------------------ scratch
+// Chunk partials of kf_decode_step_no_alloc: a fixed array in device memory
+// that the runtime sets up with the code object on each device, so that the
+// call allocates nothing.  Host code never uses the array's name as an
+// address: the per-device address comes from hipGetSymbolAddress.
+static __device__ __align__(256) unsigned char scratch[KF_SCRATCH_BYTES];
+
+namespace {
+constexpr int kScratchDevices = 64;
+std::atomic<void*> g_scratch_ptr[kScratchDevices];
+std::mutex g_scratch_mu;
+}  // namespace
+
+hipError_t scratch_address(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kScratchDevices) return hipErrorInvalidDevice;
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      if (e != hipSuccess) return e;
+      if (!p) return hipErrorInvalidSymbol;
+      g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return hipSuccess;
+}
 
 hipError_t launch_append(const AppendArgs& a, bool fp8, hipStream_t stream) {
   if (a.num_seqs == 0) return hipSuccess;

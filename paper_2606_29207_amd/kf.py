@@ -27,6 +27,8 @@ ERR_HIP = -4
 ERR_CAPACITY = -5
 ERR_INFEASIBLE = -6
 ERR_HOST_MEMORY = -7
+ERR_SCRATCH_LIMIT = -8
+SCRATCH_BYTES = 32 << 20   # KF_SCRATCH_BYTES
 
 EFLAG_TAIL_FULL = 1
 EFLAG_BAD_ROUTE = 2
@@ -37,7 +39,7 @@ KV_HEAD_MAJOR = 1
 # every symbol include/kf.h declares
 EXPORTS = ("kf_kv_append", "kf_partial_attn_workspace_bytes", "kf_partial_attn_plan",
            "kf_partial_attn", "kf_partial_attn_subset", "kf_merge_partials", "kf_decode_step",
-           "kf_debug_gather", "kf_status_str", "kf_version")
+           "kf_decode_step_no_alloc", "kf_debug_gather", "kf_status_str", "kf_version")
 
 
 class KFError(RuntimeError):
@@ -87,6 +89,9 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.kf_decode_step.argtypes = [sp, vp, vp, vp, vp, vp, vp, vp, vp, i32, vp, i32, vp, vp, vp, vp,
                                    vp, vp, vp, sz, vp, vp]
     lib.kf_decode_step.restype = ctypes.c_int
+    lib.kf_decode_step_no_alloc.argtypes = [sp, vp, vp, vp, vp, vp, vp, vp, vp, i32, vp, i32, vp,
+                                            vp, vp, vp, vp, vp, vp, vp]
+    lib.kf_decode_step_no_alloc.restype = ctypes.c_int
     lib.kf_debug_gather.argtypes = [sp, vp, vp, vp, i32, i32, i32, vp, i32, vp, vp, vp, vp]
     lib.kf_debug_gather.restype = ctypes.c_int
     lib.kf_status_str.argtypes = [ctypes.c_int]
@@ -283,14 +288,15 @@ def decode_step(shape: Shape, q, k_pool, v_pool, k_new, v_new, routes, tail_rout
                 max_pages_per_route, page_ids, seq_route_begin, o_part, lse_part, out, lse_out,
                 workspace, err_flags, k_scale=None, v_scale=None, stream=None):
     """kf_decode_step: append -> partial attention -> merge in one call (two
-    launches).  Arguments as for kv_append, partial_attn and
-    merge_partials."""
+    launches).  Arguments as for kv_append, partial_attn and merge_partials.
+    workspace=None calls kf_decode_step_no_alloc, which uses the library's
+    per-device scratch array instead."""
     lib = load()
     for t, n in ((q, "q"), (k_pool, "k_pool"), (v_pool, "v_pool"), (k_new, "k_new"),
                  (v_new, "v_new"), (routes, "routes"), (tail_route, "tail_route"),
                  (page_ids, "page_ids"), (seq_route_begin, "seq_route_begin"), (o_part, "o_part"),
                  (lse_part, "lse_part"), (out, "out"), (lse_out, "lse_out"),
-                 (workspace, "workspace"), (err_flags, "err_flags")):
+                 (err_flags, "err_flags")) + (() if workspace is None else ((workspace, "workspace"),)):
         _dev(t, n)
     B, Hq, H, R = shape.num_seqs, shape.num_q_heads, shape.num_kv_heads, routes.shape[0]
     _need(tuple(q.shape) == (B, Hq, HEAD_DIM) and q.element_size() == 2,
@@ -311,14 +317,18 @@ def decode_step(shape: Shape, q, k_pool, v_pool, k_new, v_new, routes, tail_rout
             _dev(t, n)
             _need(t.dtype == torch.float32 and t.numel() >= shape.num_pages * shape.num_kv_heads,
                   f"{n} must be float32 [num_pages, num_kv_heads]")
-    st = lib.kf_decode_step(ctypes.byref(shape), _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(k_scale),
-                            _ptr(v_scale), _ptr(k_new), _ptr(v_new), _ptr(routes), R,
-                            _ptr(tail_route), int(max_pages_per_route), _ptr(page_ids),
-                            _ptr(seq_route_begin), _ptr(o_part), _ptr(lse_part), _ptr(out),
-                            _ptr(lse_out), _ptr(workspace),
-                            workspace.numel() * workspace.element_size(), _ptr(err_flags),
-                            _stream(stream))
-    _check(st, "kf_decode_step")
+    common = (ctypes.byref(shape), _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(k_scale),
+              _ptr(v_scale), _ptr(k_new), _ptr(v_new), _ptr(routes), R, _ptr(tail_route),
+              int(max_pages_per_route), _ptr(page_ids), _ptr(seq_route_begin), _ptr(o_part),
+              _ptr(lse_part), _ptr(out), _ptr(lse_out))
+    if workspace is None:
+        st = lib.kf_decode_step_no_alloc(*common, _ptr(err_flags), _stream(stream))
+        _check(st, "kf_decode_step_no_alloc")
+    else:
+        st = lib.kf_decode_step(*common, _ptr(workspace),
+                                workspace.numel() * workspace.element_size(), _ptr(err_flags),
+                                _stream(stream))
+        _check(st, "kf_decode_step")
 
 
 def debug_gather(shape: Shape, k_pool, v_pool, routes, route, max_pages_per_route, page_ids,

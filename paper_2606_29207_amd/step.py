@@ -110,6 +110,14 @@ class DecodeState:
                        self.seq_route_begin, self.o_part, self.lse_part, self.out, self.lse,
                        self.workspace, self.err_flags, self.k_scale, self.v_scale, stream)
 
+    def step_no_alloc(self, k_new: torch.Tensor, v_new: torch.Tensor, stream=None):
+        """step_fused through kf_decode_step_no_alloc: the library's
+        per-device scratch array instead of this state's workspace."""
+        kf.decode_step(self.shape, self.q, self.k_pool, self.v_pool, k_new, v_new, self.routes,
+                       self.tail_route, self.max_pages_per_route, self.page_ids,
+                       self.seq_route_begin, self.o_part, self.lse_part, self.out, self.lse,
+                       None, self.err_flags, self.k_scale, self.v_scale, stream)
+
     # ----------------------------------------------------- query-first step
     def setup_query_first(self):
         """Split the routes into historical ones and the tails (read from the

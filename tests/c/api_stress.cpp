@@ -126,6 +126,18 @@ hipError_t launch_merge(const MergeArgs& a, hipStream_t) {
   return g_fail_launch ? hipErrorInvalidValue : hipSuccess;
 }
 
+// The scratch array of kf_decode_step_no_alloc: a host buffer of its size,
+// made the checked workspace of the call that asks for it.
+static std::vector<unsigned char> scratch_buf;
+hipError_t scratch_address(void** out) {
+  if (scratch_buf.empty()) scratch_buf.resize(KF_SCRATCH_BYTES + 256);
+  uintptr_t base = ((uintptr_t)scratch_buf.data() + 255) & ~(uintptr_t)255;
+  g_ws = reinterpret_cast<unsigned char*>(base);
+  g_ws_bytes = KF_SCRATCH_BYTES;
+  *out = g_ws;
+  return hipSuccess;
+}
+
 hipError_t launch_gather(const PartialArgs& a, bool, int route, int max_tokens, void* out_k,
                          void* out_v, hipStream_t) {
   ++g_launches;
@@ -231,6 +243,13 @@ static int call_step(const Call& c) {
                         (const int32_t*)c.pids, (const int32_t*)c.srb, (float*)c.o, (float*)c.lse,
                         (float*)c.out, (float*)c.lse_out, c.ws, c.wsb, (int32_t*)c.flags, nullptr);
 }
+static int call_step_no_alloc(const Call& c) {
+  return kf_decode_step_no_alloc(&c.s, c.q, c.k, c.v, (float*)c.ks, (float*)c.vs, c.kn, c.vn,
+                                 (kf_route*)c.routes, c.R, (const int32_t*)c.tail, c.maxp,
+                                 (const int32_t*)c.pids, (const int32_t*)c.srb, (float*)c.o,
+                                 (float*)c.lse, (float*)c.out, (float*)c.lse_out,
+                                 (int32_t*)c.flags, nullptr);
+}
 static int call_append(const Call& c) {
   return kf_kv_append(&c.s, c.k, c.v, (float*)c.ks, (float*)c.vs, c.kn, c.vn, (kf_route*)c.routes,
                       c.R, (const int32_t*)c.tail, (const int32_t*)c.pids, (int32_t*)c.flags,
@@ -248,7 +267,7 @@ static int call_gather(const Call& c) {
                          (int32_t*)c.flags, nullptr);
 }
 
-static bool known_status(int st) { return st <= 0 && st >= KF_ERR_HOST_MEMORY; }
+static bool known_status(int st) { return st <= 0 && st >= KF_ERR_SCRATCH_LIMIT; }
 
 // ---------------------------------------------------------------- checks
 typedef int (*Entry)(const Call&);
@@ -262,6 +281,13 @@ static const EntryInfo kEntries[] = {
     {"kf_partial_attn", call_partial, -1, true}, {"kf_partial_attn_subset", call_subset, -1, true},
     {"kf_decode_step", call_step, 2, true},      {"kf_kv_append", call_append, 1, false},
     {"kf_merge_partials", call_merge, 1, false}, {"kf_debug_gather", call_gather, 1, false},
+};
+// with the no-alloc step, whose valid calls may be refused for size (above)
+static const EntryInfo kMutEntries[] = {
+    {"kf_partial_attn", call_partial, -1, true}, {"kf_partial_attn_subset", call_subset, -1, true},
+    {"kf_decode_step", call_step, 2, true},      {"kf_kv_append", call_append, 1, false},
+    {"kf_merge_partials", call_merge, 1, false}, {"kf_debug_gather", call_gather, 1, false},
+    {"kf_decode_step_no_alloc", call_step_no_alloc, 2, false},
 };
 
 static void valid_calls(int iters) {
@@ -285,6 +311,41 @@ static void valid_calls(int iters) {
       g_ws = nullptr;
     }
   }
+}
+
+// kf_decode_step_no_alloc on valid arguments: KF_OK and two launches when the
+// launch's workspace need fits the scratch array, else KF_ERR_SCRATCH_LIMIT
+// before anything is launched.
+static void valid_no_alloc(int iters) {
+  long fits = 0, refused = 0;
+  for (int it = 0; it < iters; ++it) {
+    g_device = (int)rnd(0, 7);
+    Call c = valid_call();
+    int32_t cp = 0, mc = 0, up = 0;
+    CHECK(kf_partial_attn_plan(&c.s, c.R, c.maxp, 0, &cp, &mc, &up) == KF_OK, "plan");
+    const size_t need =
+        kf::workspace_layout(c.R, c.s.num_kv_heads, c.s.num_q_heads / c.s.num_kv_heads, mc).total;
+    g_launches = 0;
+    g_ws = nullptr;
+    const int st = call_step_no_alloc(c);
+    if (need <= KF_SCRATCH_BYTES) {
+      CHECK(st == KF_OK && g_launches == 2, "no-alloc step -> %d, %d launches (need %zu)", st,
+            g_launches, need);
+      ++fits;
+    } else {
+      CHECK(st == KF_ERR_SCRATCH_LIMIT && g_launches == 0, "no-alloc step over the limit -> %d",
+            st);
+      ++refused;
+    }
+    g_fail_launch = true;
+    const int st2 = call_step_no_alloc(c);
+    g_fail_launch = false;
+    CHECK(st2 == (need <= KF_SCRATCH_BYTES ? KF_ERR_HIP : KF_ERR_SCRATCH_LIMIT),
+          "refused launch -> %d", st2);
+    g_ws = nullptr;
+  }
+  CHECK(fits > 0 && refused > 0, "no-alloc sweep saw %ld fitting and %ld refused launches", fits,
+        refused);
 }
 
 // One broken argument at a time: the status the header documents, no launch.
@@ -349,9 +410,10 @@ static void one_mutation(int iters) {
   };
   for (int it = 0; it < iters; ++it) {
     g_device = (int)rnd(0, 7);
-    for (const EntryInfo& e : kEntries) {
-      const bool attn = e.fn == call_partial || e.fn == call_subset || e.fn == call_step;
-      const bool step = e.fn == call_step;
+    for (const EntryInfo& e : kMutEntries) {
+      const bool no_alloc = e.fn == call_step_no_alloc;
+      const bool attn = e.fn == call_partial || e.fn == call_subset || e.fn == call_step || no_alloc;
+      const bool step = e.fn == call_step || no_alloc;
       const bool append = e.fn == call_append;
       const bool merge = e.fn == call_merge;
       auto run = [&](const Mut& m) {
@@ -392,6 +454,12 @@ static void one_mutation(int iters) {
           else if (e.fn == call_gather)
             st = kf_debug_gather(none, cc.k, cc.v, (kf_route*)cc.routes, cc.R, 0, cc.maxp,
                                  (int32_t*)cc.pids, 1, cc.o, cc.out, (int32_t*)cc.flags, nullptr);
+          else if (e.fn == call_step_no_alloc)
+            st = kf_decode_step_no_alloc(none, cc.q, cc.k, cc.v, nullptr, nullptr, cc.kn, cc.vn,
+                                         (kf_route*)cc.routes, cc.R, (int32_t*)cc.tail, cc.maxp,
+                                         (int32_t*)cc.pids, (int32_t*)cc.srb, (float*)cc.o,
+                                         (float*)cc.lse, (float*)cc.out, (float*)cc.lse_out,
+                                         (int32_t*)cc.flags, nullptr);
           else if (e.fn == call_subset)
             st = kf_partial_attn_subset(none, cc.q, cc.k, cc.v, nullptr, nullptr,
                                         (kf_route*)cc.routes, cc.R, (int32_t*)cc.list, cc.nlist,
@@ -420,6 +488,7 @@ static void one_mutation(int iters) {
       if (attn)
         for (const Mut& m : attn_muts) {
           if (step && strstr(m.what, "65536")) continue;  // merge grid limit differs; below
+          if (no_alloc && strstr(m.what, "workspace")) continue;  // takes no workspace
           run(m);
         }
       if (step || append)
@@ -491,9 +560,10 @@ static void fuzz(int iters) {
     c.nlist = any();
     c.wsb = coin(0.5) ? (size_t)rnd(0, 1 << 30) : (size_t)-1;
     g_ws = nullptr;
-    for (const EntryInfo& e : kEntries) {
+    for (const EntryInfo& e : kMutEntries) {
       const int st = e.fn(c);
       CHECK(known_status(st), "%s fuzz status %d", e.name, st);
+      g_ws = nullptr;
     }
     int32_t cp = 0, mc = 0, up = 0;
     const int st = kf_partial_attn_plan(coin(0.05) ? nullptr : &c.s, c.R, c.maxp,
@@ -571,6 +641,7 @@ static double plans(int iters) {
 int main(int argc, char** argv) {
   const int iters = argc > 1 ? atoi(argv[1]) : 200;
   valid_calls(iters);
+  valid_no_alloc(iters * 4);
   one_mutation(iters / 4 + 1);
   fuzz(iters * 20);
   const double worst = plans(iters);

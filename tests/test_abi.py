@@ -52,7 +52,7 @@ def test_struct_layouts_match_header():
 def test_status_strings(lib):
     for code, text in ((0, "ok"), (-1, "invalid argument"), (-2, "unsupported"),
                        (-3, "workspace"), (-4, "HIP"), (-5, "too small"), (-6, "infeasible"),
-                       (-7, "host memory")):
+                       (-7, "host memory"), (-8, "scratch")):
         assert text in kf.status_str(code)
     assert kf.status_str(12345) == "unknown status"
 
@@ -390,3 +390,23 @@ def test_plan_invariants_over_random_shapes(lib):
             -(-units * m * group * 128 * 4 // 256) * 256
         if routes <= 200:   # the sizing loop is linear in the table's routes
             assert kf.partial_attn_workspace_bytes(s, routes, maxp) >= need
+
+
+def test_no_alloc_step_refuses_launches_beyond_its_scratch(lib):
+    """kf_decode_step_no_alloc checks every argument first, then refuses a
+    launch whose split units need more than KF_SCRATCH_BYTES of scratch,
+    before anything is launched: 100 routes x 8 KV heads x a group of 16, up
+    to 1000 pages, split into 9 ranges, need 59.9 MB."""
+    from paper_2606_29207_amd import kf as k
+    assert k.SCRATCH_BYTES == 32 << 20
+    s = _shape(num_seqs=16, num_q_heads=128, num_kv_heads=8, num_pages=10 ** 6,
+               num_page_ids=100 * 1000)
+    assert k.partial_attn_plan(s, 100, 1000)[1] == 9
+    v = lambda x: ctypes.c_void_p(x)  # noqa: E731
+    args = [ctypes.byref(s), v(FAKE), v(FAKE), v(FAKE), None, None, v(FAKE), v(FAKE), v(FAKE), 100,
+            v(FAKE), 1000, v(FAKE), v(FAKE), v(FAKE), v(FAKE), v(FAKE), v(FAKE), v(FAKE), None]
+    assert lib.kf_decode_step_no_alloc(*args) == k.ERR_SCRATCH_LIMIT
+    assert "KF_SCRATCH_BYTES" in k.status_str(k.ERR_SCRATCH_LIMIT)
+    bad = list(args)
+    bad[16] = None                                      # null out: an argument error comes first
+    assert lib.kf_decode_step_no_alloc(*bad) == k.ERR_INVALID_ARG
