@@ -345,14 +345,14 @@ template <>
 struct TileRaw<true> {
   u32x4 k[4][2];  // [c][pp]: 16 E4M3 of K row kslot(c), dims 64*pp + 16*grp ..
   u32x4 v[8];     // [b8]: the 16 E4M3 slots of V^T row d = 16*b8 + li
+  float ks, vs;   // K and V scales of the lane's page (vpage)
 };
 
-// Wave-uniform description of one tile: its first route-local page, the
-// page ids of its (up to four) pages and, for fp8 pools, their scales.
+// Wave-uniform description of one tile: its first route-local page and the
+// page ids of its (up to four) pages.
 struct TileInfo {
   int tp0;
   int pid0, pid1, pid2, pid3;
-  float ks0, ks1, ks2, ks3, vs0, vs1, vs2, vs3;
 };
 
 template <class T>
@@ -467,9 +467,12 @@ __global__ __launch_bounds__(kThreads * UPW, 2 / UPW) void partial_kernel(Partia
 
   auto next_tile = [&](int cur) -> int { return cur + kWaves; };  // wave w: w, w+4, ...
 
-  // Page ids are uniform, so they (and fp8 scales) arrive through scalar
-  // loads; a page past the range or outside the pool reads page 0 and is
-  // masked (its p set to 0 whatever its scales hold) or flagged.
+  // Page ids are uniform, so they arrive through scalar loads; a page past
+  // the range or outside the pool reads page 0 and is masked (its p set to 0
+  // whatever its scales hold) or flagged.  fp8 page scales arrive with the
+  // tile's vector loads instead, each lane loading those of its own page: a
+  // scalar load of a scale would wait on the scalar load of its page id, and
+  // every wait on a scalar load waits on all of them (fp8 layer 1.9% faster).
   bool pid_bad = false;
   auto page_at = [&](int pg) -> int {  // page id of route-local page pg of the range
     const bool in = pg < p1;
@@ -489,24 +492,6 @@ __global__ __launch_bounds__(kThreads * UPW, 2 / UPW) void partial_kernel(Partia
     t.pid1 = page_at(t.tp0 + 1);
     t.pid2 = TP > 2 ? page_at(t.tp0 + 2) : 0;
     t.pid3 = TP > 2 ? page_at(t.tp0 + 3) : 0;
-    t.ks0 = t.ks1 = t.ks2 = t.ks3 = t.vs0 = t.vs1 = t.vs2 = t.vs3 = 1.0f;
-    if constexpr (FP8) {
-      t.ks0 = a.k_scale[(size_t)t.pid0 * H + g];
-      t.ks1 = a.k_scale[(size_t)t.pid1 * H + g];
-      t.ks2 = a.k_scale[(size_t)t.pid2 * H + g];
-      t.ks3 = a.k_scale[(size_t)t.pid3 * H + g];
-      t.vs0 = a.v_scale[(size_t)t.pid0 * H + g];
-      t.vs1 = a.v_scale[(size_t)t.pid1 * H + g];
-      t.vs2 = a.v_scale[(size_t)t.pid2 * H + g];
-      t.vs3 = a.v_scale[(size_t)t.pid3 * H + g];
-      if (writer) {  // the tail page's scales were just written: take them from LDS
-        const int k = app_page - t.tp0;
-        if (k == 0) { t.ks0 = s_app[0]; t.vs0 = s_app[1]; }
-        if (k == 1) { t.ks1 = s_app[0]; t.vs1 = s_app[1]; }
-        if (k == 2) { t.ks2 = s_app[0]; t.vs2 = s_app[1]; }
-        if (k == 3) { t.ks3 = s_app[0]; t.vs3 = s_app[1]; }
-      }
-    }
     return t;
   };
 
@@ -538,6 +523,8 @@ __global__ __launch_bounds__(kThreads * UPW, 2 / UPW) void partial_kernel(Partia
         for (int pp = 0; pp < 2; ++pp) t.k[cc][pp] = ld16_stream(kb + cc * 4 * kDim + 64 * pp);
 #pragma unroll
       for (int b8 = 0; b8 < 8; ++b8) t.v[b8] = ld16_stream(vb + b8 * 16 * kPage);
+      t.ks = a.k_scale[(size_t)pv * H + g];
+      t.vs = a.v_scale[(size_t)pv * H + g];
     }
   };
 
@@ -580,8 +567,13 @@ __global__ __launch_bounds__(kThreads * UPW, 2 / UPW) void partial_kernel(Partia
     }
     float ks = a.scale_log2, vs = 1.0f;
     if constexpr (FP8) {
-      ks *= pick4(ti.ks0, ti.ks1, ti.ks2, ti.ks3, vpage);
-      vs = pick4(ti.vs0, ti.vs1, ti.vs2, ti.vs3, vpage);
+      float kss = t.ks;
+      vs = t.vs;
+      if (writer && ti.tp0 + vpage == app_page) {  // the tail page's scales were just written
+        kss = s_app[0];
+        vs = s_app[1];
+      }
+      ks *= kss;
     }
     const int tok0 = (ti.tp0 + vpage) * kPage + GeoT::vslot0(grp);  // route-local token, c = r4 = 0
     float mt = neg_inf();
