@@ -704,8 +704,17 @@ __global__ __launch_bounds__(kThreads * UPW, 2 / UPW) void partial_kernel(Partia
   }
   __syncthreads();
   if (tid < G) {
+    // a NaN wave max (a bad page) makes the unit's max NaN: fmaxf would skip
+    // it, and a range whose waves are all bad would then read as empty (-inf)
+    // and be dropped by the combine instead of poisoning the unit
     float M = neg_inf();
-    for (int ww = 0; ww < kWaves; ++ww) M = fmaxf(M, s_m[ww][tid]);
+    bool nan_m = false;
+    for (int ww = 0; ww < kWaves; ++ww) {
+      const float mw = s_m[ww][tid];
+      nan_m |= mw != mw;
+      M = fmaxf(M, mw);
+    }
+    if (nan_m) M = qnan();
     float L = 0.0f;
     for (int ww = 0; ww < kWaves; ++ww) {
       const float mw = s_m[ww][tid];
@@ -716,7 +725,7 @@ __global__ __launch_bounds__(kThreads * UPW, 2 / UPW) void partial_kernel(Partia
     s_fm[tid] = M;
     s_fl[tid] = L;
   }
-  if (tid == 0 && wave_bad) atomicOr(a.err_flags, KF_EFLAG_BAD_PAGE);
+  if (lane == 0 && wave_bad) atomicOr(a.err_flags, KF_EFLAG_BAD_PAGE);  // whichever wave saw it
   __syncthreads();
   if (!work) return;  // after the workgroup's last barrier
 

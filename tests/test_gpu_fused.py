@@ -183,3 +183,22 @@ def test_fused_fp8_reencode_of_pages_begun_by_appends(gpu):
     o = run_oracle(inst, 24, new_tokens=tokens)
     for key in ("routes", "k_pool", "v_pool", "k_scale", "v_scale"):
         assert np.array_equal(f[key], o[key]), key
+
+
+@pytest.mark.parametrize("page", [1, 2, 5, 9, 30])
+def test_bad_page_in_any_wave_raises_the_flag(gpu, page):
+    """A page id outside the pool, at local pages that fall to different
+    waves (each wave takes every fourth 2-page tile, from a per-route
+    rotation), and a broken route row: NaN for the unit and its sequence,
+    BAD_PAGE and BAD_ROUTE raised whichever wave loads the bad page, the rest
+    as the oracle has it; the fused step equals the three calls."""
+    wl = workload("llama8b_32k", num_seqs=3, num_q_heads=8, num_kv_heads=2, part_tokens=600,
+                  appends=1)
+    inst = make_instance(wl, seed=9, steps=2, seq_lens=[1300, 700, 1000])
+    inst.routes[1, 3] = inst.routes[1, 2] - 5          # tok_end < tok_begin
+    inst.page_ids[int(inst.routes[3, 4]) + page] = inst.num_pages + 7
+    o = run_oracle(inst, 2)
+    assert o["flags"] == oracle.EFLAG_BAD_ROUTE | oracle.EFLAG_BAD_PAGE
+    f = host(run_gpu(inst, 2, fused=True))
+    compare_all(f, o)
+    same_bits(f, host(run_gpu(inst, 2)))
