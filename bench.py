@@ -391,8 +391,9 @@ def main(argv=None):
     t_step = np.array([e[0].elapsed_time(e[3]) for e in ev]) * 1e3
     # attention + merge: the two calls, or (query-first) the whole overlapped step
     t_am = t_step if qf else t_par + t_mrg
-    # the committed counter profiles were taken on page-major pools
-    traffic = counter_traffic(wl.name, args.seed) if args.kv_layout == "page" else None
+    # the committed counter profiles were taken on page-major pools, for the
+    # partial call over the whole route table (not the query-first launch)
+    traffic = counter_traffic(wl.name, args.seed) if args.kv_layout == "page" and not qf else None
     out = {
         "metric": METRIC,
         "value": round(step_b / (us_step * 1e-6) / 1e9, 2),
