@@ -145,8 +145,11 @@ int kf_kv_append(const kf_shape* shape, void* k_pool, void* v_pool, float* k_sca
  * current device (at least 256 bytes).  One workgroup handles a whole
  * (route, KV head) unit when there are enough units to fill the GPU; with
  * fewer, each unit is split over several workgroups whose partials go through
- * this workspace.  The size covers every launch of at most `num_routes`
- * routes, so a workspace sized for a route table also serves
+ * this workspace; a split launch of at least two rounds of resident
+ * workgroups also keeps its dispatch order there (8 bytes per work item, a
+ * table that a one-workgroup kernel writes before the partial kernel).  The
+ * size covers every launch of at most `num_routes` routes, so a workspace
+ * sized for a route table also serves
  * kf_partial_attn_subset over any part of it, and it covers ragged and
  * equal routes alike: it does not depend on shape->num_page_ids, so it stays
  * valid as the page table grows or shrinks.  No initialisation is needed;
@@ -167,7 +170,11 @@ size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes
  *   *chunk_pages  pages per workgroup range; a unit of n pages is cut into
  *                 ceil(n / chunk_pages) ranges
  *   *max_chunks   most ranges per unit; 1 = every unit whole, no combine
- *                 launch and no workspace use
+ *                 launch and no workspace use.  A split launch whose
+ *                 max_chunks * num_kv_heads * num_launch work items reach
+ *                 two per resident workgroup slot (two slots per compute
+ *                 unit) and stay within 2^20 is dispatched largest ranges
+ *                 first, in an order a one-workgroup kernel computes
  *   *units_per_wg 1 or 2 (route, KV head) units per workgroup
  * The plan reads the launch size, the KV heads and dtype, the device's
  * compute units, max_pages_per_route and shape->num_page_ids: a page table
@@ -251,10 +258,12 @@ int kf_merge_partials(int32_t num_seqs, int32_t num_routes, int32_t num_q_heads,
  *   kf_kv_append -> kf_partial_attn -> kf_merge_partials
  * on the same arguments (each argument as documented there; the workspace
  * is sized by kf_partial_attn_workspace_bytes), in two launches instead of
- * three: the workgroup that attends over a tail's last page first writes the
- * step's token into it (for fp8 pools by the E4M3 append rule, re-encoding
- * the page if needed) and attends over it, and the merge advances the tails'
- * tok_end and raises the append's flags.  All host checks of the three calls
+ * three (a split launch adds its combine and, over several rounds, its
+ * dispatch order, as kf_partial_attn does): the workgroup that attends over
+ * a tail's last page first writes the step's token into it (for fp8 pools
+ * by the E4M3 append rule, re-encoding the page if needed) and attends over
+ * it, and the merge advances the tails' tok_end and raises the append's
+ * flags.  All host checks of the three calls
  * are made before anything is launched.
  */
 int kf_decode_step(const kf_shape* shape, const void* q, void* k_pool, void* v_pool,

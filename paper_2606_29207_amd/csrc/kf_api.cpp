@@ -153,13 +153,22 @@ int32_t units_per_workgroup(bool fp8, bool route_list, const ChunkPlan& plan, in
              : 1;
 }
 
+bool ordered_dispatch(const ChunkPlan& plan, int32_t num_launch, int32_t num_kv_heads,
+                      int64_t slots) {
+  const int64_t items = (int64_t)plan.max_chunks * num_kv_heads * num_launch;
+  return plan.max_chunks > 1 && items >= 2 * slots && items <= kMaxOrderItems;
+}
+
 WorkspaceLayout workspace_layout(int32_t num_routes, int32_t num_kv_heads, int32_t group,
-                                 int32_t max_chunks) {
+                                 int32_t max_chunks, bool ordered) {
   WorkspaceLayout l;
-  const size_t recs = max_chunks > 1 ? (size_t)num_routes * num_kv_heads * max_chunks * group : 0;
+  const size_t units = (size_t)num_routes * num_kv_heads * max_chunks;
+  const size_t recs = max_chunks > 1 ? units * group : 0;
   l.ml_off = 0;
   l.o_off = round_up(recs * 2 * sizeof(float), 256);
-  l.total = l.o_off + round_up(recs * kDim * sizeof(float), 256);
+  l.order_off = l.o_off + round_up(recs * kDim * sizeof(float), 256);
+  l.total = l.order_off + (ordered ? round_up((2 + 2 * units) * sizeof(uint32_t), 256) : 0);
+  if (!ordered) l.order_off = 0;
   if (l.total < 256) l.total = 256;
   return l;
 }
@@ -205,7 +214,10 @@ size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes
     for (const bool ragged : {false, true}) {
       const kf::ChunkPlan plan =
           kf::plan_for_slots(m, shape->num_kv_heads, max_pages_per_route, ragged, fp8, slots);
-      const size_t t = kf::workspace_layout(m, shape->num_kv_heads, group, plan.max_chunks).total;
+      const size_t t =
+          kf::workspace_layout(m, shape->num_kv_heads, group, plan.max_chunks,
+                               kf::ordered_dispatch(plan, m, shape->num_kv_heads, slots))
+              .total;
       if (t > most) most = t;
     }
   }
@@ -302,8 +314,10 @@ int prepare_partial(const kf_shape* shape, const void* q, const void* k_pool, co
       num_launch, shape->num_kv_heads, max_pages_per_route,
       kf::ragged_table(shape->num_page_ids, num_launch, max_pages_per_route),
       shape->kv_dtype == KF_KV_FP8_E4M3);
+  const bool ordered =
+      kf::ordered_dispatch(plan, num_launch, shape->num_kv_heads, 2 * (int64_t)kf::cu_count());
   const kf::WorkspaceLayout l =
-      kf::workspace_layout(num_launch, shape->num_kv_heads, group, plan.max_chunks);
+      kf::workspace_layout(num_launch, shape->num_kv_heads, group, plan.max_chunks, ordered);
   if (!workspace || !aligned(workspace, 256) || workspace_bytes < l.total) return KF_ERR_WORKSPACE;
 
   a.q = static_cast<const uint16_t*>(q);
@@ -319,6 +333,7 @@ int prepare_partial(const kf_shape* shape, const void* q, const void* k_pool, co
   char* ws = static_cast<char*>(workspace);
   a.ws_ml = reinterpret_cast<float*>(ws + l.ml_off);
   a.ws_o = reinterpret_cast<float*>(ws + l.o_off);
+  a.order = ordered ? reinterpret_cast<uint32_t*>(ws + l.order_off) : nullptr;
   a.err_flags = err_flags;
   a.num_seqs = shape->num_seqs;
   a.num_q_heads = shape->num_q_heads;
@@ -422,6 +437,8 @@ int decode_step_impl(const kf_shape* shape, const void* q, void* k_pool, void* v
     const uintptr_t b = reinterpret_cast<uintptr_t>(base), s0 = reinterpret_cast<uintptr_t>(kStandIn);
     pa.ws_ml = reinterpret_cast<float*>(b + (reinterpret_cast<uintptr_t>(pa.ws_ml) - s0));
     pa.ws_o = reinterpret_cast<float*>(b + (reinterpret_cast<uintptr_t>(pa.ws_o) - s0));
+    if (pa.order)
+      pa.order = reinterpret_cast<uint32_t*>(b + (reinterpret_cast<uintptr_t>(pa.order) - s0));
   }
   const hipStream_t s = as_stream(stream);
   const bool fp8 = shape->kv_dtype == KF_KV_FP8_E4M3;

@@ -18,6 +18,8 @@ constexpr int kWaves = 4;             // waves per unit (a workgroup, or half of
 constexpr int kMinSplitPages = 16;    // smallest page range a split workgroup gets
 constexpr int kMaxPagesTwoUnit = 2048;  // longest units run two per workgroup (bf16, unsplit)
 constexpr int kMaxLaunchRoutes = 65535;  // routes per launch and KV heads: grid dimension limits
+constexpr int kOrderBuckets = 64;        // range-size classes of the dispatch order
+constexpr int64_t kMaxOrderItems = int64_t(1) << 20;  // largest split launch given a dispatch order
 
 struct AppendArgs {
   void* k_pool;
@@ -53,6 +55,11 @@ struct PartialArgs {
   int32_t num_units_routes;  // routes launched: num_list, or num_routes without a list
   int32_t chunk_pages, max_chunks;  // a unit of n pages uses ceil(n / chunk_pages) workgroups
   int32_t units_per_wg;  // 2: unsplit bf16 launch, two units per 512-thread workgroup
+  // Split launches of several rounds: the dispatch order of the work items,
+  // written by order_kernel before the partial kernel runs (NULL: grid
+  // order).  [0] the item count, [1] unused, then per item (launch position
+  // u, KV head << 16 | range index).
+  uint32_t* order;
   int32_t head_major;    // pools [Hkv][num_pages][...] instead of [num_pages][Hkv][...]
   int32_t num_pages, num_page_ids;
   float scale_log2;     // scale * log2(e): scores are kept in the base-2 domain
@@ -86,7 +93,7 @@ struct MergeArgs {
 };
 
 struct WorkspaceLayout {
-  size_t ml_off, o_off, total;
+  size_t ml_off, o_off, order_off, total;  // order_off: 0 without a dispatch order
 };
 
 // How the pages of each (route, KV head) unit are spread over workgroups.
@@ -111,8 +118,13 @@ ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_page
 // (1 or 2); route_list: a launch over a route list (kf_partial_attn_subset).
 int32_t units_per_workgroup(bool fp8, bool route_list, const ChunkPlan& plan, int32_t num_launch,
                             int32_t num_kv_heads, int32_t max_pages_per_route);
+// A split launch of at least two rounds of the GPU's `slots` resident
+// workgroups (and at most kMaxOrderItems work items) runs its work items
+// in a computed order, largest ranges first (order_kernel).
+bool ordered_dispatch(const ChunkPlan& plan, int32_t num_launch, int32_t num_kv_heads,
+                      int64_t slots);
 WorkspaceLayout workspace_layout(int32_t num_routes, int32_t num_kv_heads, int32_t group,
-                                 int32_t max_chunks);
+                                 int32_t max_chunks, bool ordered);
 
 // Address of the current device's scratch array (KF_SCRATCH_BYTES, for
 // kf_decode_step_no_alloc), looked up once per device.

@@ -2,6 +2,8 @@
 // (KernelFlume, arXiv 2606.29207, Section 3.2 steps 3-4, Section 5.1):
 //   append_kernel   -- tail append of the step's K/V token
 //   partial_kernel  -- local attention over token-range routes -> (o, lse)
+//   order_kernel    -- dispatch order of a split launch of several rounds
+//   combine_kernel  -- in-range reduction of a split unit's ranges
 //   merge_kernel    -- log-sum-exp merge of the partials of each sequence
 //
 // partial_kernel is HBM-bound (4 flop per KV byte at 4 query heads per KV
@@ -399,8 +401,19 @@ __global__ __launch_bounds__(kThreads * UPW, 2 / UPW) void partial_kernel(Partia
   auto& s_fl = s_fl_u[half];
   float* s_app = s_app_u[half];
 
-  const int c = blockIdx.x;
+  int c = blockIdx.x;
   int g = blockIdx.y, u = blockIdx.z + half * gridDim.z;  // u: position in the launch
+  if (UPW == 1 && a.order) {
+    // a split launch of several rounds: take the work item of this
+    // workgroup's place in the dispatch order; places past the last item
+    // have no work
+    const uint32_t i = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+    if (i >= a.order[0]) return;
+    const uint32_t e0 = a.order[2 + 2 * (size_t)i], e1 = a.order[3 + 2 * (size_t)i];
+    u = (int)e0;
+    g = (int)(e1 >> 16);
+    c = (int)(e1 & 0xFFFFu);
+  }
   if constexpr (FP8) {
     // Unsplit fp8 units: workgroups are dealt round-robin over the 8 XCDs.
     // Give XCD k the k-th eighth of the (head, route) space instead, so the
@@ -771,6 +784,66 @@ __global__ __launch_bounds__(kThreads * UPW, 2 / UPW) void partial_kernel(Partia
   }
 }
 
+// The dispatch order of a split launch of several rounds.  The hardware
+// deals the workgroups of a launch in order over the XCDs and, within an
+// XCD, round-robin over its shader engines, and an XCD stops dealing at a
+// workgroup whose engine has no free slot: a run of long ranges on one
+// engine then idles the others.  Work items (launch position u, KV head,
+// range) are therefore listed largest range first (64 size classes), so
+// neighbouring workgroups hold ranges of about the same length, and units
+// that need no range (empty or bad routes) keep one item for their outputs.
+// Which workgroup computes an item does not change any result.  One
+// workgroup; the order within a size class follows LDS atomics.
+__global__ __launch_bounds__(1024) void order_kernel(PartialArgs a) {
+  __shared__ uint32_t s_count[kOrderBuckets];
+  __shared__ uint32_t s_next[kOrderBuckets];
+  const int tid = threadIdx.x, H = a.num_kv_heads, U = a.num_units_routes;
+  if (tid < kOrderBuckets) s_count[tid] = 0;
+  __syncthreads();
+  // ranges of unit u and the size class of its ranges (0: the largest)
+  auto unit = [&](int u, int& k, int& cls) {
+    const int r = a.route_list ? a.route_list[u] : u;
+    k = 1;
+    int size = 0;
+    if (r >= 0 && r < a.num_routes) {
+      const RouteView rv = read_route(a, r);
+      if (!rv.bad && rv.npages > 0) {
+        k = (rv.npages + a.chunk_pages - 1) / a.chunk_pages;
+        size = (rv.npages + k - 1) / k;
+      }
+    }
+    const int64_t q = (int64_t)size * kOrderBuckets / ((int64_t)a.chunk_pages + 1);
+    cls = kOrderBuckets - 1 - (int)(q < kOrderBuckets - 1 ? q : kOrderBuckets - 1);
+  };
+  for (int u = tid; u < U; u += blockDim.x) {
+    int k, cls;
+    unit(u, k, cls);
+    atomicAdd(&s_count[cls], (uint32_t)(k * H));
+  }
+  __syncthreads();
+  if (tid == 0) {
+    uint32_t run = 0;
+    for (int b = 0; b < kOrderBuckets; ++b) {
+      s_next[b] = run;
+      run += s_count[b];
+    }
+    a.order[0] = run;
+    a.order[1] = 0;
+  }
+  __syncthreads();
+  for (int u = tid; u < U; u += blockDim.x) {
+    int k, cls;
+    unit(u, k, cls);
+    const uint32_t pos = atomicAdd(&s_next[cls], (uint32_t)(k * H));
+    for (int g = 0; g < H; ++g)
+      for (int c = 0; c < k; ++c) {
+        const size_t i = pos + (size_t)g * k + c;
+        a.order[2 + 2 * i] = (uint32_t)u;
+        a.order[3 + 2 * i] = ((uint32_t)g << 16) | (uint32_t)c;
+      }
+  }
+}
+
 // Combine the chunk partials of each chunked (route, KV head) in chunk order.
 // Wave w reduces heads w, w+4, ...: its lanes read up to 64 chunks' (max,
 // sum) at once; then every thread sums its output elements over the chunks
@@ -1010,6 +1083,11 @@ hipError_t launch_partial(const PartialArgs& a, bool fp8, hipStream_t stream) {
     return launch_partial_kernel<false, 2>(a, dim3(1, a.num_kv_heads, (a.num_units_routes + 1) / 2),
                                            stream);
   const dim3 grid(a.max_chunks, a.num_kv_heads, a.num_units_routes);
+  if (a.order) {
+    hipLaunchKernelGGL(order_kernel, dim3(1), dim3(1024), 0, stream, a);
+    const hipError_t eo = hipGetLastError();
+    if (eo != hipSuccess) return eo;
+  }
   hipError_t e = fp8 ? launch_partial_kernel<true, 1>(a, grid, stream)
                      : launch_partial_kernel<false, 1>(a, grid, stream);
   if (e != hipSuccess || a.max_chunks == 1) return e;

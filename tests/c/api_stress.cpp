@@ -45,6 +45,13 @@ hipError_t hipDeviceGetAttribute(int* value, hipDeviceAttribute_t attr, int devi
   return hipSuccess;
 }
 
+// Whether a launch with this plan runs in a computed dispatch order on the
+// current fake device (two resident workgroups per CU).
+static int64_t fake_slots() { return 2 * (int64_t)(g_no_device ? 256 : kCus[g_device]); }
+static bool ordered(int32_t cp, int32_t mc, int32_t routes, int32_t heads) {
+  return kf::ordered_dispatch(kf::ChunkPlan{cp, mc}, routes, heads, fake_slots());
+}
+
 // ------------------------------------------------------- launch checkers
 static int g_launches = 0;
 static bool g_fail_launch = false;
@@ -112,6 +119,21 @@ hipError_t launch_partial(const PartialArgs& a, bool fp8, hipStream_t) {
     if (g_ws)
       CHECK((unsigned char*)(a.ws_o + recs * kDim) <= g_ws + g_ws_bytes,
             "workspace needs %zu records, has %zu bytes", recs, g_ws_bytes);
+  }
+  const size_t items = (size_t)a.num_units_routes * a.num_kv_heads * a.max_chunks;
+  CHECK(!a.order == !kf::ordered_dispatch(kf::ChunkPlan{a.chunk_pages, a.max_chunks},
+                                          a.num_units_routes, a.num_kv_heads, fake_slots()),
+        "dispatch order %p for %zu items", (const void*)a.order, items);
+  if (a.order) {
+    CHECK(a.max_chunks > 1 && a.units_per_wg == 1, "dispatch order of an unsplit launch");
+    const size_t recs = items * a.group;
+    touch(a.order);
+    touch(a.order + 2 + 2 * items - 1);
+    CHECK((const unsigned char*)a.order >= (const unsigned char*)(a.ws_o + recs * kDim),
+          "dispatch order over the records");
+    if (g_ws)
+      CHECK((unsigned char*)(a.order + 2 + 2 * items) <= g_ws + g_ws_bytes,
+            "dispatch order of %zu items past the workspace of %zu bytes", items, g_ws_bytes);
   }
   return g_fail_launch ? hipErrorInvalidValue : hipSuccess;
 }
@@ -324,7 +346,9 @@ static void valid_no_alloc(int iters) {
     int32_t cp = 0, mc = 0, up = 0;
     CHECK(kf_partial_attn_plan(&c.s, c.R, c.maxp, 0, &cp, &mc, &up) == KF_OK, "plan");
     const size_t need =
-        kf::workspace_layout(c.R, c.s.num_kv_heads, c.s.num_q_heads / c.s.num_kv_heads, mc).total;
+        kf::workspace_layout(c.R, c.s.num_kv_heads, c.s.num_q_heads / c.s.num_kv_heads, mc,
+                             ordered(cp, mc, c.R, c.s.num_kv_heads))
+            .total;
     g_launches = 0;
     g_ws = nullptr;
     const int st = call_step_no_alloc(c);
@@ -503,7 +527,8 @@ static void one_mutation(int iters) {
         if (kf_partial_attn_plan(&c.s, c.R, c.maxp, 0, &cp, &mc, &up) == KF_OK && mc > 1) {
           attach_workspace(c, c.R);
           const size_t need = kf::workspace_layout(c.R, c.s.num_kv_heads,
-                                                   c.s.num_q_heads / c.s.num_kv_heads, mc)
+                                                   c.s.num_q_heads / c.s.num_kv_heads, mc,
+                                                   ordered(cp, mc, c.R, c.s.num_kv_heads))
                                   .total;
           c.wsb = need - 256;
           g_launches = 0;
@@ -607,7 +632,8 @@ static double plans(int iters) {
               cp, maxp);
         if (up == 2) CHECK(list == 0 && mc == 1 && s.kv_dtype == KF_KV_BF16, "two-unit mode");
         const size_t need = kf::workspace_layout(m, s.num_kv_heads,
-                                                 s.num_q_heads / s.num_kv_heads, mc)
+                                                 s.num_q_heads / s.num_kv_heads, mc,
+                                                 ordered(cp, mc, m, s.num_kv_heads))
                                 .total;
         CHECK(need <= ws, "launch of %d routes needs %zu > queried %zu (R=%d maxp=%d H=%d)", m,
               need, ws, R, maxp, s.num_kv_heads);

@@ -186,7 +186,9 @@ def _workspace_need(units_routes, H, G, maxp, ragged, slots=512, fp8=False):
     slots; 6 for fp8 pools) or about one per slot (fewer; four when ragged),
     never under 16
     pages, an odd chunk count for the longest unit except for one per slot;
-    records of (max, sum) and o per query head, each array rounded up to 256
+    records of (max, sum) and o per query head, and, for a split launch of
+    at least two rounds (up to 2^20 work items), a dispatch-order table of
+    two words per item after a two-word header, each array rounded up to 256
     bytes."""
     rup = lambda x: -(-x // 256) * 256  # noqa: E731
     units = units_routes * H
@@ -207,7 +209,9 @@ def _workspace_need(units_routes, H, G, maxp, ragged, slots=512, fp8=False):
             cc -= 1
             tries += 1
     recs = units * m * G
-    return rup(recs * 2 * 4) + rup(recs * 128 * 4)
+    items = units * m                       # (route, KV head, range) work items of the launch
+    ordered = m > 1 and 2 * slots <= items <= 1 << 20
+    return rup(recs * 2 * 4) + rup(recs * 128 * 4) + (rup((2 + 2 * items) * 4) if ordered else 0)
 
 
 def test_workspace_bytes(lib):

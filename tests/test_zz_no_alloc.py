@@ -54,6 +54,11 @@ def test_no_alloc_step_equals_decode_step_twice(gpu):
     small = make_instance(workload("wide_gqa_fp8_decode", num_seqs=2, num_q_heads=16,
                                    num_kv_heads=2, part_tokens=1024), seed=4, steps=2,
                           seq_lens=[2500, 700])
+    import torch
     p1 = _step_pair(big)
+    # the first launch runs in a computed dispatch order (a table in the scratch array)
+    slots = 2 * torch.cuda.get_device_properties(0).multi_processor_count
+    items = p1[1] * big.wl.num_kv_heads * len(big.routes)
+    assert 2 * slots <= items <= 1 << 20, f"plan {p1}: {items} work items"
     p2 = _step_pair(small)
     print(f"[no_alloc] plans {p1} then {p2}", flush=True)
