@@ -793,11 +793,17 @@ __global__ __launch_bounds__(kThreads * UPW, 2 / UPW) void partial_kernel(Partia
 // neighbouring workgroups hold ranges of about the same length, and units
 // that need no range (empty or bad routes) keep one item for their outputs.
 // Which workgroup computes an item does not change any result.  One
-// workgroup; the order within a size class follows LDS atomics.
+// workgroup; the order within a size class follows LDS atomics.  Up to
+// kOrderLdsUnits units keep their range count and class in LDS between the
+// two passes (more read their routes again).
+constexpr int kOrderLdsUnits = 16384;
 __global__ __launch_bounds__(1024) void order_kernel(PartialArgs a) {
   __shared__ uint32_t s_count[kOrderBuckets];
   __shared__ uint32_t s_next[kOrderBuckets];
+  __shared__ uint16_t s_k[kOrderLdsUnits];
+  __shared__ uint8_t s_cls[kOrderLdsUnits];
   const int tid = threadIdx.x, H = a.num_kv_heads, U = a.num_units_routes;
+  const bool keep = U <= kOrderLdsUnits;
   if (tid < kOrderBuckets) s_count[tid] = 0;
   __syncthreads();
   // ranges of unit u and the size class of its ranges (0: the largest)
@@ -819,6 +825,10 @@ __global__ __launch_bounds__(1024) void order_kernel(PartialArgs a) {
     int k, cls;
     unit(u, k, cls);
     atomicAdd(&s_count[cls], (uint32_t)(k * H));
+    if (keep) {
+      s_k[u] = (uint16_t)k;   // k <= max_chunks <= 65535
+      s_cls[u] = (uint8_t)cls;
+    }
   }
   __syncthreads();
   if (tid == 0) {
@@ -833,7 +843,12 @@ __global__ __launch_bounds__(1024) void order_kernel(PartialArgs a) {
   __syncthreads();
   for (int u = tid; u < U; u += blockDim.x) {
     int k, cls;
-    unit(u, k, cls);
+    if (keep) {
+      k = s_k[u];
+      cls = s_cls[u];
+    } else {
+      unit(u, k, cls);
+    }
     const uint32_t pos = atomicAdd(&s_next[cls], (uint32_t)(k * H));
     for (int g = 0; g < H; ++g)
       for (int c = 0; c < k; ++c) {
