@@ -228,6 +228,9 @@ def policy_report(inst, wl, bw_gbps: float, attn_us: float, hbm_bytes: int) -> d
                            "T_step = layers x measured attention+merge, T_prewarm 1 s"}
 
 
+ORDER_MAX_ITEMS = 1 << 20   # largest split launch given a dispatch order
+
+
 def kernel_label(st, wl, route_list=None) -> str:
     """The partial-attention launch the timed step makes (route_list: a launch
     over those routes), from the library's own plan: its kernel, units per
@@ -241,6 +244,13 @@ def kernel_label(st, wl, route_list=None) -> str:
         name += f" over {n} listed routes"
     if max_chunks > 1:
         name += f" + combine_kernel ({chunk_pages}-page chunks, up to {max_chunks} per unit)"
+        # split launches of at least two rounds of resident workgroups (two per CU) run
+        # largest ranges first, in an order the one-workgroup order_kernel writes
+        import torch
+        slots = 2 * torch.cuda.get_device_properties(0).multi_processor_count
+        items = max_chunks * st.shape.num_kv_heads * n
+        if 2 * slots <= items <= ORDER_MAX_ITEMS:
+            name = "order_kernel + " + name
     return name
 
 
