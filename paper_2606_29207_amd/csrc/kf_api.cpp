@@ -98,6 +98,12 @@ ChunkPlan plan_for_slots(int32_t num_routes, int32_t num_kv_heads, int32_t max_p
   const int64_t target = (units < slots ? (ragged ? 4 : 1) : many) * slots;
   int64_t c = (units * max_pages_per_route + target - 1) / target;  // < 2^31 * 2^15
   if (c < kMinSplitPages) c = kMinSplitPages;
+  // With at least a round of bf16 units, ranges of fewer than
+  // kMinRangePagesMany pages cost more in each workgroup's start and finish
+  // than they gain in balance (960 units of 256 pages: 40-page ranges 331 us,
+  // whole units 307 us; 512 ragged units: 94-page ranges 630 us, 205-page
+  // ranges 605 us).  fp8 launches measured no gain from such a floor.
+  if (!fp8 && units >= slots && c < kMinRangePagesMany) c = kMinRangePagesMany;
   if (c >= max_pages_per_route) return {whole, 1};
   int64_t m = (max_pages_per_route + c - 1) / c;
   // Workgroups are dealt round-robin over the 8 XCDs in launch order, chunk

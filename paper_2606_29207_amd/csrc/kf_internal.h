@@ -16,6 +16,7 @@ constexpr int kPage = KF_PAGE_SIZE;   // tokens per page
 constexpr int kDim = KF_HEAD_DIM;     // head dimension
 constexpr int kWaves = 4;             // waves per unit (a workgroup, or half of one)
 constexpr int kMinSplitPages = 16;    // smallest page range a split workgroup gets
+constexpr int kMinRangePagesMany = 256;  // ... in bf16 launches of at least a round of units
 constexpr int kMaxPagesTwoUnit = 2048;  // longest units run two per workgroup (bf16, unsplit)
 constexpr int kMaxLaunchRoutes = 65535;  // routes per launch and KV heads: grid dimension limits
 constexpr int kOrderBuckets = 64;        // range-size classes of the dispatch order

@@ -183,9 +183,8 @@ def _workspace_need(units_routes, H, G, maxp, ragged, slots=512, fp8=False):
     units that fill whole rounds of the resident slots stay whole (no
     records) unless the routes are ragged (a page table under 90% of routes
     x max pages); otherwise chunks of about 12 per slot (more units than
-    slots; 6 for fp8 pools) or about one per slot (fewer; four when ragged),
-    never under 16
-    pages, an odd chunk count for the longest unit except for one per slot;
+    slots, never under 256 pages; 6 for fp8 pools) or about one per slot
+    (fewer; four when ragged), never under 16 pages, an odd chunk count for the longest unit except for one per slot;
     records of (max, sum) and o per query head, and, for a split launch of
     at least two rounds (up to 2^20 work items), a dispatch-order table of
     two words per item after a two-word header, each array rounded up to 256
@@ -196,6 +195,8 @@ def _workspace_need(units_routes, H, G, maxp, ragged, slots=512, fp8=False):
         return 256
     target = ((6 if fp8 else 12) if units >= slots else 4 if ragged else 1) * slots
     c = max(-(-units * maxp // target), 16)
+    if units >= slots and not fp8:
+        c = max(c, 256)                     # at least a round of bf16 units: ranges of >= 256 pages
     if c >= maxp:
         return 256
     m = -(-maxp // c)
@@ -291,7 +292,8 @@ def test_partial_attn_plan(lib):
     bf16t = _shape(num_seqs=20, num_q_heads=64, num_kv_heads=8, num_pages=81920,
                    num_page_ids=81920)
     assert plan(fp8t, 80, 1024) == (214, 5, 1)               # 640 units: ~6 ranges per slot
-    assert plan(bf16t, 80, 1024) == (94, 11, 1)              # ... and ~12 for bf16
+    assert plan(bf16t, 80, 1024) == (205, 5, 1)             # ... and ~12 for bf16, but ranges
+    #                                                         of >= 256 pages (then an odd count)
     for pids in (100, 81920):
         sh = _shape(num_seqs=20, num_q_heads=64, num_kv_heads=8, kv_dtype=kf.KV_FP8_E4M3,
                     num_pages=10, num_page_ids=pids)
@@ -399,15 +401,15 @@ def test_plan_invariants_over_random_shapes(lib):
 def test_no_alloc_step_refuses_launches_beyond_its_scratch(lib):
     """kf_decode_step_no_alloc checks every argument first, then refuses a
     launch whose split units need more than KF_SCRATCH_BYTES of scratch,
-    before anything is launched: 100 routes x 8 KV heads x a group of 16, up
-    to 1000 pages, split into 9 ranges, need 59.9 MB."""
+    before anything is launched: 200 routes x 8 KV heads x a group of 16, up
+    to 1000 pages, split into 5 ranges, need 66.6 MB."""
     from paper_2606_29207_amd import kf as k
     assert k.SCRATCH_BYTES == 32 << 20
     s = _shape(num_seqs=16, num_q_heads=128, num_kv_heads=8, num_pages=10 ** 6,
-               num_page_ids=100 * 1000)
-    assert k.partial_attn_plan(s, 100, 1000)[1] == 9
+               num_page_ids=200 * 1000)
+    assert k.partial_attn_plan(s, 200, 1000)[1] == 5
     v = lambda x: ctypes.c_void_p(x)  # noqa: E731
-    args = [ctypes.byref(s), v(FAKE), v(FAKE), v(FAKE), None, None, v(FAKE), v(FAKE), v(FAKE), 100,
+    args = [ctypes.byref(s), v(FAKE), v(FAKE), v(FAKE), None, None, v(FAKE), v(FAKE), v(FAKE), 200,
             v(FAKE), 1000, v(FAKE), v(FAKE), v(FAKE), v(FAKE), v(FAKE), v(FAKE), v(FAKE), None]
     assert lib.kf_decode_step_no_alloc(*args) == k.ERR_SCRATCH_LIMIT
     assert "KF_SCRATCH_BYTES" in k.status_str(k.ERR_SCRATCH_LIMIT)

@@ -77,7 +77,7 @@ def test_ordered_route_list_launch(gpu):
     from paper_2606_29207_amd import kf
     from paper_2606_29207_amd.step import DecodeState
     lens = [(i * 997) % 9000 + 100 for i in range(80)]
-    inst = make_instance(workload("agentic_mix", num_seqs=len(lens), part_tokens=4096, appends=0),
+    inst = make_instance(workload("agentic_mix", num_seqs=len(lens), part_tokens=8192, appends=0),
                          seed=22, steps=1, seq_lens=lens)
     st = DecodeState.from_instance(inst)
     R = len(inst.routes)
