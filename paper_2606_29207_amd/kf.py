@@ -119,9 +119,20 @@ def _ptr(t: torch.Tensor | None):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
+# the current stream's raw handle without building a torch.cuda.Stream object
+# (a few microseconds per call through the public API)
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+_cur_device = getattr(torch._C, "_cuda_getDevice", None)
+
+
 def _stream(stream):
-    s = torch.cuda.current_stream() if stream is None else stream
-    return ctypes.c_void_p(s.cuda_stream)
+    """hipStream_t of `stream` (a torch stream), or of the current torch
+    stream when None, as an integer for a c_void_p argument."""
+    if stream is not None:
+        return stream.cuda_stream
+    if _raw_stream is not None and _cur_device is not None:
+        return _raw_stream(_cur_device())
+    return torch.cuda.current_stream().cuda_stream
 
 
 def _dev(t: torch.Tensor, name: str, dtype=None):
@@ -173,31 +184,99 @@ def shape_of(q, k_pool, page_ids, scale, kv_layout=None) -> Shape:
                       kv_layout)
 
 
-def kv_append(shape: Shape, k_pool, v_pool, k_new, v_new, routes, tail_route, page_ids,
-              err_flags, stream=None, k_scale=None, v_scale=None):
-    """kf_kv_append.  routes: int32 [R, 6] (updated in place); fp8 pools also
-    take (and update) k_scale/v_scale float32 [P, Hkv]."""
-    lib = load()
-    for t, n in ((k_pool, "k_pool"), (v_pool, "v_pool"), (k_new, "k_new"), (v_new, "v_new"),
-                 (routes, "routes"), (tail_route, "tail_route"), (page_ids, "page_ids"),
-                 (err_flags, "err_flags")):
-        _dev(t, n)
-    B, H = shape.num_seqs, shape.num_kv_heads
-    _need(tuple(k_new.shape) == (B, H, HEAD_DIM) and tuple(v_new.shape) == (B, H, HEAD_DIM),
-          "k_new/v_new must be [num_seqs, num_kv_heads, 128]")
-    _need(k_new.element_size() == 2 and v_new.element_size() == 2, "k_new/v_new must be bf16")
-    _need(tail_route.numel() >= B and tail_route.dtype == torch.int32, "tail_route: int32 [num_seqs]")
-    _check_tables(shape, k_pool, v_pool, routes, page_ids)
+class BoundCall:
+    """An entry point with its arguments checked and marshalled once.
+
+    Calling it issues the C call again with the same device pointers, on
+    ``stream`` (the current torch stream when None).  It holds a reference
+    to every tensor it was bound to, so those pointers stay valid while the
+    object lives: writes into the tensors between calls are seen; a tensor
+    replaced elsewhere is not.  A per-step decode loop pays the argument
+    checks once instead of on every step (tens of microseconds of host time
+    against a few microseconds of kernel time for small batches)."""
+
+    __slots__ = ("_fn", "_what", "_args", "_keep")
+
+    def __init__(self, fn, what: str, args, keep):
+        self._fn, self._what, self._args, self._keep = fn, what, tuple(args), tuple(keep)
+
+    def __call__(self, stream=None):
+        st = self._fn(*self._args, _stream(stream))
+        if st != 0:
+            _check(st, self._what)
+
+
+class BoundTokenCall(BoundCall):
+    """A BoundCall whose entry point also takes the step's new token: k_new
+    and v_new (bf16 device tensors [num_seqs, num_kv_heads, 128]) are given
+    per call and checked against the bound shape."""
+
+    __slots__ = ("_tok_at", "_tok_shape")
+
+    def __init__(self, fn, what: str, args, keep, tok_at: int, tok_shape):
+        super().__init__(fn, what, args, keep)
+        self._tok_at, self._tok_shape = tok_at, torch.Size(tok_shape)
+
+    def __call__(self, k_new, v_new, stream=None):
+        for t, n in ((k_new, "k_new"), (v_new, "v_new")):
+            if not (isinstance(t, torch.Tensor) and t.is_cuda and t.shape == self._tok_shape
+                    and t.element_size() == 2 and t.is_contiguous()):
+                raise KFError(f"{n} must be a contiguous bf16 device tensor "
+                              f"{list(self._tok_shape)}")
+        i, a = self._tok_at, self._args
+        st = self._fn(*a[:i], k_new.data_ptr(), v_new.data_ptr(), *a[i:], _stream(stream))
+        if st != 0:
+            _check(st, self._what)
+
+
+def _copy_shape(shape: Shape) -> Shape:
+    return Shape.from_buffer_copy(shape)
+
+
+def _check_scales(shape: Shape, k_scale, v_scale):
     if shape.kv_dtype == KV_FP8_E4M3:
         for t, n in ((k_scale, "k_scale"), (v_scale, "v_scale")):
             _need(t is not None, f"{n} is required for fp8 pools")
             _dev(t, n)
             _need(t.dtype == torch.float32 and t.numel() >= shape.num_pages * shape.num_kv_heads,
                   f"{n} must be float32 [num_pages, num_kv_heads]")
-    st = lib.kf_kv_append(ctypes.byref(shape), _ptr(k_pool), _ptr(v_pool), _ptr(k_scale),
-                          _ptr(v_scale), _ptr(k_new), _ptr(v_new), _ptr(routes), routes.shape[0],
-                          _ptr(tail_route), _ptr(page_ids), _ptr(err_flags), _stream(stream))
-    _check(st, "kf_kv_append")
+
+
+def _check_tokens(shape: Shape, k_new, v_new):
+    _dev(k_new, "k_new")
+    _dev(v_new, "v_new")
+    B, H = shape.num_seqs, shape.num_kv_heads
+    _need(tuple(k_new.shape) == (B, H, HEAD_DIM) and tuple(v_new.shape) == (B, H, HEAD_DIM),
+          "k_new/v_new must be [num_seqs, num_kv_heads, 128]")
+    _need(k_new.element_size() == 2 and v_new.element_size() == 2, "k_new/v_new must be bf16")
+
+
+def bind_kv_append(shape: Shape, k_pool, v_pool, routes, tail_route, page_ids, err_flags,
+                   k_scale=None, v_scale=None) -> BoundTokenCall:
+    """kf_kv_append bound to its tables; call it as (k_new, v_new, stream)."""
+    lib = load()
+    for t, n in ((k_pool, "k_pool"), (v_pool, "v_pool"), (routes, "routes"),
+                 (tail_route, "tail_route"), (page_ids, "page_ids"), (err_flags, "err_flags")):
+        _dev(t, n)
+    B, H = shape.num_seqs, shape.num_kv_heads
+    _need(tail_route.numel() >= B and tail_route.dtype == torch.int32, "tail_route: int32 [num_seqs]")
+    _check_tables(shape, k_pool, v_pool, routes, page_ids)
+    _check_scales(shape, k_scale, v_scale)
+    sh = _copy_shape(shape)
+    args = (ctypes.byref(sh), _ptr(k_pool), _ptr(v_pool), _ptr(k_scale), _ptr(v_scale),
+            _ptr(routes), routes.shape[0], _ptr(tail_route), _ptr(page_ids), _ptr(err_flags))
+    return BoundTokenCall(lib.kf_kv_append, "kf_kv_append", args,
+                          (sh, k_pool, v_pool, k_scale, v_scale, routes, tail_route, page_ids,
+                           err_flags), 5, (B, H, HEAD_DIM))
+
+
+def kv_append(shape: Shape, k_pool, v_pool, k_new, v_new, routes, tail_route, page_ids,
+              err_flags, stream=None, k_scale=None, v_scale=None):
+    """kf_kv_append.  routes: int32 [R, 6] (updated in place); fp8 pools also
+    take (and update) k_scale/v_scale float32 [P, Hkv]."""
+    _check_tokens(shape, k_new, v_new)
+    bind_kv_append(shape, k_pool, v_pool, routes, tail_route, page_ids, err_flags,
+                   k_scale, v_scale)(k_new, v_new, stream)
 
 
 def partial_attn_workspace_bytes(shape: Shape, num_routes: int, max_pages_per_route: int) -> int:
@@ -223,12 +302,12 @@ def alloc_workspace(shape: Shape, num_routes: int, max_pages_per_route: int, dev
     return torch.zeros(n, dtype=torch.uint8, device=device)
 
 
-def partial_attn(shape: Shape, q, k_pool, v_pool, routes, max_pages_per_route, page_ids,
-                 o_part, lse_part, workspace, err_flags, k_scale=None, v_scale=None,
-                 stream=None, route_list=None):
+def bind_partial_attn(shape: Shape, q, k_pool, v_pool, routes, max_pages_per_route, page_ids,
+                      o_part, lse_part, workspace, err_flags, k_scale=None, v_scale=None,
+                      route_list=None) -> BoundCall:
     """kf_partial_attn (all routes) or, with ``route_list`` (int32 device
-    tensor of route indices), kf_partial_attn_subset.
-    o_part float32 [R, Hq, 128], lse_part float32 [R, Hq]."""
+    tensor of route indices), kf_partial_attn_subset, bound to its buffers;
+    call it as (stream).  o_part float32 [R, Hq, 128], lse_part float32 [R, Hq]."""
     lib = load()
     for t, n in ((q, "q"), (k_pool, "k_pool"), (v_pool, "v_pool"), (routes, "routes"),
                  (page_ids, "page_ids"), (o_part, "o_part"), (lse_part, "lse_part"),
@@ -242,31 +321,37 @@ def partial_attn(shape: Shape, q, k_pool, v_pool, routes, max_pages_per_route, p
     _need(tuple(o_part.shape) == (R, shape.num_q_heads, HEAD_DIM), "o_part must be [R, Hq, 128]")
     _need(tuple(lse_part.shape) == (R, shape.num_q_heads), "lse_part must be [R, Hq]")
     _check_tables(shape, k_pool, v_pool, routes, page_ids)
-    if shape.kv_dtype == KV_FP8_E4M3:
-        for t, n in ((k_scale, "k_scale"), (v_scale, "v_scale")):
-            _need(t is not None, f"{n} is required for fp8 pools")
-            _dev(t, n)
-            _need(t.dtype == torch.float32 and t.numel() >= shape.num_pages * shape.num_kv_heads,
-                  f"{n} must be float32 [num_pages, num_kv_heads]")
+    _check_scales(shape, k_scale, v_scale)
+    sh = _copy_shape(shape)
     ws_bytes = workspace.numel() * workspace.element_size()
-    common_tail = (int(max_pages_per_route), _ptr(page_ids), _ptr(o_part), _ptr(lse_part),
-                   _ptr(workspace), ws_bytes, _ptr(err_flags), _stream(stream))
+    head = (ctypes.byref(sh), _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(k_scale), _ptr(v_scale),
+            _ptr(routes), R)
+    tail = (int(max_pages_per_route), _ptr(page_ids), _ptr(o_part), _ptr(lse_part),
+            _ptr(workspace), ws_bytes, _ptr(err_flags))
+    keep = (sh, q, k_pool, v_pool, k_scale, v_scale, routes, page_ids, o_part, lse_part,
+            workspace, err_flags)
     if route_list is None:
-        st = lib.kf_partial_attn(ctypes.byref(shape), _ptr(q), _ptr(k_pool), _ptr(v_pool),
-                                 _ptr(k_scale), _ptr(v_scale), _ptr(routes), R, *common_tail)
-        _check(st, "kf_partial_attn")
-    else:
-        _dev(route_list, "route_list")
-        _need(route_list.dtype == torch.int32 and route_list.dim() == 1, "route_list must be int32 [n]")
-        st = lib.kf_partial_attn_subset(ctypes.byref(shape), _ptr(q), _ptr(k_pool), _ptr(v_pool),
-                                        _ptr(k_scale), _ptr(v_scale), _ptr(routes), R,
-                                        _ptr(route_list), route_list.numel(), *common_tail)
-        _check(st, "kf_partial_attn_subset")
+        return BoundCall(lib.kf_partial_attn, "kf_partial_attn", head + tail, keep)
+    _dev(route_list, "route_list")
+    _need(route_list.dtype == torch.int32 and route_list.dim() == 1, "route_list must be int32 [n]")
+    return BoundCall(lib.kf_partial_attn_subset, "kf_partial_attn_subset",
+                     head + (_ptr(route_list), route_list.numel()) + tail, keep + (route_list,))
 
 
-def merge_partials(num_seqs, o_part, lse_part, seq_route_begin, out, lse_out, err_flags,
-                   stream=None):
-    """kf_merge_partials.  out float32 [B, Hq, 128], lse_out float32 [B, Hq]."""
+def partial_attn(shape: Shape, q, k_pool, v_pool, routes, max_pages_per_route, page_ids,
+                 o_part, lse_part, workspace, err_flags, k_scale=None, v_scale=None,
+                 stream=None, route_list=None):
+    """kf_partial_attn (all routes) or, with ``route_list`` (int32 device
+    tensor of route indices), kf_partial_attn_subset.
+    o_part float32 [R, Hq, 128], lse_part float32 [R, Hq]."""
+    bind_partial_attn(shape, q, k_pool, v_pool, routes, max_pages_per_route, page_ids, o_part,
+                      lse_part, workspace, err_flags, k_scale, v_scale, route_list)(stream)
+
+
+def bind_merge_partials(num_seqs, o_part, lse_part, seq_route_begin, out, lse_out,
+                        err_flags) -> BoundCall:
+    """kf_merge_partials bound to its buffers; call it as (stream).
+    out float32 [B, Hq, 128], lse_out float32 [B, Hq]."""
     lib = load()
     for t, n in ((o_part, "o_part"), (lse_part, "lse_part"), (seq_route_begin, "seq_route_begin"),
                  (out, "out"), (lse_out, "lse_out"), (err_flags, "err_flags")):
@@ -278,10 +363,55 @@ def merge_partials(num_seqs, o_part, lse_part, seq_route_begin, out, lse_out, er
           "seq_route_begin must be int32 [num_seqs + 1]")
     _need(tuple(out.shape) == (num_seqs, Hq, D) and out.dtype == torch.float32, "out must be float32 [B, Hq, D]")
     _need(tuple(lse_out.shape) == (num_seqs, Hq) and lse_out.dtype == torch.float32, "lse_out must be float32 [B, Hq]")
-    st = lib.kf_merge_partials(int(num_seqs), R, Hq, D, _ptr(o_part), _ptr(lse_part),
-                               _ptr(seq_route_begin), _ptr(out), _ptr(lse_out),
-                               _ptr(err_flags), _stream(stream))
-    _check(st, "kf_merge_partials")
+    args = (int(num_seqs), R, Hq, D, _ptr(o_part), _ptr(lse_part), _ptr(seq_route_begin),
+            _ptr(out), _ptr(lse_out), _ptr(err_flags))
+    return BoundCall(lib.kf_merge_partials, "kf_merge_partials", args,
+                     (o_part, lse_part, seq_route_begin, out, lse_out, err_flags))
+
+
+def merge_partials(num_seqs, o_part, lse_part, seq_route_begin, out, lse_out, err_flags,
+                   stream=None):
+    """kf_merge_partials.  out float32 [B, Hq, 128], lse_out float32 [B, Hq]."""
+    bind_merge_partials(num_seqs, o_part, lse_part, seq_route_begin, out, lse_out,
+                        err_flags)(stream)
+
+
+def bind_decode_step(shape: Shape, q, k_pool, v_pool, routes, tail_route, max_pages_per_route,
+                     page_ids, seq_route_begin, o_part, lse_part, out, lse_out, workspace,
+                     err_flags, k_scale=None, v_scale=None) -> BoundTokenCall:
+    """kf_decode_step bound to its buffers; call it as (k_new, v_new, stream).
+    workspace=None binds kf_decode_step_no_alloc, which uses the library's
+    per-device scratch array instead."""
+    lib = load()
+    for t, n in ((q, "q"), (k_pool, "k_pool"), (v_pool, "v_pool"), (routes, "routes"),
+                 (tail_route, "tail_route"), (page_ids, "page_ids"),
+                 (seq_route_begin, "seq_route_begin"), (o_part, "o_part"),
+                 (lse_part, "lse_part"), (out, "out"), (lse_out, "lse_out"),
+                 (err_flags, "err_flags")) + (() if workspace is None else ((workspace, "workspace"),)):
+        _dev(t, n)
+    B, Hq, H, R = shape.num_seqs, shape.num_q_heads, shape.num_kv_heads, routes.shape[0]
+    _need(tuple(q.shape) == (B, Hq, HEAD_DIM) and q.element_size() == 2,
+          "q must be bf16 [num_seqs, num_q_heads, 128]")
+    _need(tail_route.numel() >= B and tail_route.dtype == torch.int32, "tail_route: int32 [num_seqs]")
+    _need(seq_route_begin.dtype == torch.int32 and seq_route_begin.numel() >= B + 1,
+          "seq_route_begin must be int32 [num_seqs + 1]")
+    for t, shp, n in ((o_part, (R, Hq, HEAD_DIM), "o_part"), (lse_part, (R, Hq), "lse_part"),
+                      (out, (B, Hq, HEAD_DIM), "out"), (lse_out, (B, Hq), "lse_out")):
+        _need(tuple(t.shape) == shp and t.dtype == torch.float32, f"{n} must be float32 {list(shp)}")
+    _check_tables(shape, k_pool, v_pool, routes, page_ids)
+    _check_scales(shape, k_scale, v_scale)
+    sh = _copy_shape(shape)
+    args = (ctypes.byref(sh), _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(k_scale), _ptr(v_scale),
+            _ptr(routes), R, _ptr(tail_route), int(max_pages_per_route), _ptr(page_ids),
+            _ptr(seq_route_begin), _ptr(o_part), _ptr(lse_part), _ptr(out), _ptr(lse_out))
+    keep = (sh, q, k_pool, v_pool, k_scale, v_scale, routes, tail_route, page_ids,
+            seq_route_begin, o_part, lse_part, out, lse_out, err_flags)
+    if workspace is None:
+        return BoundTokenCall(lib.kf_decode_step_no_alloc, "kf_decode_step_no_alloc",
+                              args + (_ptr(err_flags),), keep, 6, (B, H, HEAD_DIM))
+    return BoundTokenCall(lib.kf_decode_step, "kf_decode_step",
+                          args + (_ptr(workspace), workspace.numel() * workspace.element_size(),
+                                  _ptr(err_flags)), keep + (workspace,), 6, (B, H, HEAD_DIM))
 
 
 def decode_step(shape: Shape, q, k_pool, v_pool, k_new, v_new, routes, tail_route,
@@ -291,44 +421,10 @@ def decode_step(shape: Shape, q, k_pool, v_pool, k_new, v_new, routes, tail_rout
     launches).  Arguments as for kv_append, partial_attn and merge_partials.
     workspace=None calls kf_decode_step_no_alloc, which uses the library's
     per-device scratch array instead."""
-    lib = load()
-    for t, n in ((q, "q"), (k_pool, "k_pool"), (v_pool, "v_pool"), (k_new, "k_new"),
-                 (v_new, "v_new"), (routes, "routes"), (tail_route, "tail_route"),
-                 (page_ids, "page_ids"), (seq_route_begin, "seq_route_begin"), (o_part, "o_part"),
-                 (lse_part, "lse_part"), (out, "out"), (lse_out, "lse_out"),
-                 (err_flags, "err_flags")) + (() if workspace is None else ((workspace, "workspace"),)):
-        _dev(t, n)
-    B, Hq, H, R = shape.num_seqs, shape.num_q_heads, shape.num_kv_heads, routes.shape[0]
-    _need(tuple(q.shape) == (B, Hq, HEAD_DIM) and q.element_size() == 2,
-          "q must be bf16 [num_seqs, num_q_heads, 128]")
-    _need(tuple(k_new.shape) == (B, H, HEAD_DIM) and tuple(v_new.shape) == (B, H, HEAD_DIM)
-          and k_new.element_size() == 2 and v_new.element_size() == 2,
-          "k_new/v_new must be bf16 [num_seqs, num_kv_heads, 128]")
-    _need(tail_route.numel() >= B and tail_route.dtype == torch.int32, "tail_route: int32 [num_seqs]")
-    _need(seq_route_begin.dtype == torch.int32 and seq_route_begin.numel() >= B + 1,
-          "seq_route_begin must be int32 [num_seqs + 1]")
-    for t, shp, n in ((o_part, (R, Hq, HEAD_DIM), "o_part"), (lse_part, (R, Hq), "lse_part"),
-                      (out, (B, Hq, HEAD_DIM), "out"), (lse_out, (B, Hq), "lse_out")):
-        _need(tuple(t.shape) == shp and t.dtype == torch.float32, f"{n} must be float32 {list(shp)}")
-    _check_tables(shape, k_pool, v_pool, routes, page_ids)
-    if shape.kv_dtype == KV_FP8_E4M3:
-        for t, n in ((k_scale, "k_scale"), (v_scale, "v_scale")):
-            _need(t is not None, f"{n} is required for fp8 pools")
-            _dev(t, n)
-            _need(t.dtype == torch.float32 and t.numel() >= shape.num_pages * shape.num_kv_heads,
-                  f"{n} must be float32 [num_pages, num_kv_heads]")
-    common = (ctypes.byref(shape), _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(k_scale),
-              _ptr(v_scale), _ptr(k_new), _ptr(v_new), _ptr(routes), R, _ptr(tail_route),
-              int(max_pages_per_route), _ptr(page_ids), _ptr(seq_route_begin), _ptr(o_part),
-              _ptr(lse_part), _ptr(out), _ptr(lse_out))
-    if workspace is None:
-        st = lib.kf_decode_step_no_alloc(*common, _ptr(err_flags), _stream(stream))
-        _check(st, "kf_decode_step_no_alloc")
-    else:
-        st = lib.kf_decode_step(*common, _ptr(workspace),
-                                workspace.numel() * workspace.element_size(), _ptr(err_flags),
-                                _stream(stream))
-        _check(st, "kf_decode_step")
+    _check_tokens(shape, k_new, v_new)
+    bind_decode_step(shape, q, k_pool, v_pool, routes, tail_route, max_pages_per_route, page_ids,
+                     seq_route_begin, o_part, lse_part, out, lse_out, workspace, err_flags,
+                     k_scale, v_scale)(k_new, v_new, stream)
 
 
 def debug_gather(shape: Shape, k_pool, v_pool, routes, route, max_pages_per_route, page_ids,

@@ -5,7 +5,8 @@ routes and page ids) and the output buffers as torch device tensors, and runs
 one decode step as the paper orders it (Section 3.2, steps 3-4; Section 5.1):
 the tail routes append the step's K/V token, every route computes its partial,
 and the partials of each sequence are merged.  Marshalling only: the three
-calls are the library's HIP kernels, enqueued on the current stream.
+calls are the library's HIP kernels, enqueued on the current stream.  Their
+arguments are checked and marshalled once, when the state is built.
 """
 from __future__ import annotations
 
@@ -33,7 +34,14 @@ class DecodeState:
     seq_route_begin int32 [B+1]; tail_route int32 [B].  kv_layout =
     kf.KV_HEAD_MAJOR stores the (page-major) pools given here head-major on
     the device: [Hkv, P, ...].
+
+    The calls are bound to the device tensors built here (kf.BoundCall):
+    write into them between steps; replacing one raises AttributeError.
     """
+
+    _BOUND = frozenset(("q", "k_pool", "v_pool", "k_scale", "v_scale", "routes", "page_ids",
+                        "seq_route_begin", "tail_route", "workspace", "o_part", "lse_part", "out",
+                        "lse", "err_flags", "shape", "max_pages_per_route"))
 
     def __init__(self, *, q, k_pool, v_pool, routes, page_ids, seq_route_begin, tail_route,
                  scale, max_pages_per_route, k_scale=None, v_scale=None, device="cuda",
@@ -65,6 +73,33 @@ class DecodeState:
         self.out = torch.empty((B, Hq, D), dtype=torch.float32, device=device)
         self.lse = torch.empty((B, Hq), dtype=torch.float32, device=device)
         self.err_flags = torch.zeros(1, dtype=torch.int32, device=device)
+        self._append = kf.bind_kv_append(self.shape, self.k_pool, self.v_pool, self.routes,
+                                         self.tail_route, self.page_ids, self.err_flags,
+                                         self.k_scale, self.v_scale)
+        self._partial = kf.bind_partial_attn(self.shape, self.q, self.k_pool, self.v_pool,
+                                             self.routes, self.max_pages_per_route,
+                                             self.page_ids, self.o_part, self.lse_part,
+                                             self.workspace, self.err_flags, self.k_scale,
+                                             self.v_scale)
+        self._merge = kf.bind_merge_partials(self.num_seqs, self.o_part, self.lse_part,
+                                             self.seq_route_begin, self.out, self.lse,
+                                             self.err_flags)
+        self._fused = self._bind_fused(self.workspace)
+        self._no_alloc = None
+        self._frozen = True
+
+    def __setattr__(self, name, value):
+        if name in self._BOUND and self.__dict__.get("_frozen"):
+            raise AttributeError(f"DecodeState.{name} is bound into the marshalled calls: "
+                                 "write into the tensor instead of replacing it")
+        object.__setattr__(self, name, value)
+
+    def _bind_fused(self, workspace):
+        return kf.bind_decode_step(self.shape, self.q, self.k_pool, self.v_pool, self.routes,
+                                   self.tail_route, self.max_pages_per_route, self.page_ids,
+                                   self.seq_route_begin, self.o_part, self.lse_part, self.out,
+                                   self.lse, workspace, self.err_flags, self.k_scale,
+                                   self.v_scale)
 
     @classmethod
     def from_instance(cls, inst, device="cuda", kv_layout=None):
@@ -81,18 +116,13 @@ class DecodeState:
 
     # ---------------------------------------------------------------- calls
     def append(self, k_new: torch.Tensor, v_new: torch.Tensor, stream=None):
-        kf.kv_append(self.shape, self.k_pool, self.v_pool, k_new, v_new, self.routes,
-                     self.tail_route, self.page_ids, self.err_flags, stream,
-                     self.k_scale, self.v_scale)
+        self._append(k_new, v_new, stream)
 
     def partial(self, stream=None):
-        kf.partial_attn(self.shape, self.q, self.k_pool, self.v_pool, self.routes,
-                        self.max_pages_per_route, self.page_ids, self.o_part, self.lse_part,
-                        self.workspace, self.err_flags, self.k_scale, self.v_scale, stream)
+        self._partial(stream)
 
     def merge(self, stream=None):
-        kf.merge_partials(self.num_seqs, self.o_part, self.lse_part, self.seq_route_begin,
-                          self.out, self.lse, self.err_flags, stream)
+        self._merge(stream)
 
     def step(self, k_new: torch.Tensor | None = None, v_new: torch.Tensor | None = None,
              stream=None):
@@ -105,18 +135,14 @@ class DecodeState:
     def step_fused(self, k_new: torch.Tensor, v_new: torch.Tensor, stream=None):
         """One decode step through kf_decode_step: same results as step(),
         with the append fused into the partial-attention launch."""
-        kf.decode_step(self.shape, self.q, self.k_pool, self.v_pool, k_new, v_new, self.routes,
-                       self.tail_route, self.max_pages_per_route, self.page_ids,
-                       self.seq_route_begin, self.o_part, self.lse_part, self.out, self.lse,
-                       self.workspace, self.err_flags, self.k_scale, self.v_scale, stream)
+        self._fused(k_new, v_new, stream)
 
     def step_no_alloc(self, k_new: torch.Tensor, v_new: torch.Tensor, stream=None):
         """step_fused through kf_decode_step_no_alloc: the library's
         per-device scratch array instead of this state's workspace."""
-        kf.decode_step(self.shape, self.q, self.k_pool, self.v_pool, k_new, v_new, self.routes,
-                       self.tail_route, self.max_pages_per_route, self.page_ids,
-                       self.seq_route_begin, self.o_part, self.lse_part, self.out, self.lse,
-                       None, self.err_flags, self.k_scale, self.v_scale, stream)
+        if self._no_alloc is None:
+            self._no_alloc = self._bind_fused(None)
+        self._no_alloc(k_new, v_new, stream)
 
     # ----------------------------------------------------- query-first step
     def setup_query_first(self):
@@ -132,6 +158,12 @@ class DecodeState:
         self.ws_hist = kf.alloc_workspace(self.shape, R, self.max_pages_per_route, self.device)
         self.ws_tail = kf.alloc_workspace(self.shape, R, self.max_pages_per_route, self.device)
         self.stream_b = torch.cuda.Stream(device=self.device)   # default priority
+        self._qf_hist, self._qf_tail = (
+            kf.bind_partial_attn(self.shape, self.q, self.k_pool, self.v_pool, self.routes,
+                                 self.max_pages_per_route, self.page_ids, self.o_part,
+                                 self.lse_part, ws, self.err_flags, self.k_scale, self.v_scale,
+                                 route_list=lst)
+            for ws, lst in ((self.ws_hist, self.hist_list), (self.ws_tail, self.tail_list)))
         self._qf_ready = torch.cuda.Event()
         self._qf_tail_done = torch.cuda.Event()
 
@@ -148,18 +180,12 @@ class DecodeState:
         if hist_events is not None:
             hist_events[0].record(cur)
         if self.hist_list.numel():
-            kf.partial_attn(self.shape, self.q, self.k_pool, self.v_pool, self.routes,
-                            self.max_pages_per_route, self.page_ids, self.o_part, self.lse_part,
-                            self.ws_hist, self.err_flags, self.k_scale, self.v_scale, cur,
-                            route_list=self.hist_list)
+            self._qf_hist(cur)
         if hist_events is not None:
             hist_events[1].record(cur)
         self.append(k_new, v_new, self.stream_b)
         if self.tail_list.numel():
-            kf.partial_attn(self.shape, self.q, self.k_pool, self.v_pool, self.routes,
-                            self.max_pages_per_route, self.page_ids, self.o_part, self.lse_part,
-                            self.ws_tail, self.err_flags, self.k_scale, self.v_scale,
-                            self.stream_b, route_list=self.tail_list)
+            self._qf_tail(self.stream_b)
         self._qf_tail_done.record(self.stream_b)
         cur.wait_event(self._qf_tail_done)
         self.merge(cur)

@@ -379,3 +379,38 @@ def test_nan_inputs_poison_only_their_unit(gpu):
     assert np.isnan(g["out"][1]).sum() == G and np.isnan(g["o_part"][r_v]).sum() == G
     assert np.isnan(g["o_part"][r_k, 0:G]).all()
     assert np.isfinite(g["out"][2]).all() and g["flags"] == 0
+
+
+def test_bound_calls_match_the_unbound_binding(gpu):
+    """DecodeState's calls are marshalled once (kf.BoundCall): several steps
+    through them give the same bits as the same steps through the per-call
+    binding on a second copy of the state, and replacing a bound tensor is
+    refused."""
+    import torch
+    from paper_2606_29207_amd import kf
+    from paper_2606_29207_amd.step import DecodeState
+    inst = make_instance(workload("tiny", appends=1), seed=5, steps=3)
+    a, b = DecodeState.from_instance(inst), DecodeState.from_instance(inst)
+    for s in range(3):
+        kn, vn = a.upload_new_tokens(*inst.new_tokens(s))
+        (a.step_fused if s % 2 else a.step)(kn, vn)
+        if s % 2:
+            kf.decode_step(b.shape, b.q, b.k_pool, b.v_pool, kn, vn, b.routes, b.tail_route,
+                           b.max_pages_per_route, b.page_ids, b.seq_route_begin, b.o_part,
+                           b.lse_part, b.out, b.lse, b.workspace, b.err_flags)
+        else:
+            kf.kv_append(b.shape, b.k_pool, b.v_pool, kn, vn, b.routes, b.tail_route, b.page_ids,
+                         b.err_flags)
+            kf.partial_attn(b.shape, b.q, b.k_pool, b.v_pool, b.routes, b.max_pages_per_route,
+                            b.page_ids, b.o_part, b.lse_part, b.workspace, b.err_flags)
+            kf.merge_partials(b.num_seqs, b.o_part, b.lse_part, b.seq_route_begin, b.out, b.lse,
+                              b.err_flags)
+    torch.cuda.synchronize()
+    ga, gb = host(a), host(b)
+    for k in ("o_part", "lse_part", "out", "lse", "k_pool", "v_pool", "routes"):
+        assert np.array_equal(ga[k], gb[k], equal_nan=True), k
+    compare_all(ga, run_oracle(inst, 3))
+    with pytest.raises(AttributeError, match="bound"):
+        a.q = a.q.clone()
+    with pytest.raises(kf.KFError, match="k_new"):
+        a.step_fused(kn[:, :1].contiguous(), vn)
