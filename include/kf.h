@@ -85,10 +85,10 @@ typedef struct {
 } kf_shape;
 
 /* Pool layouts.  Page-major keeps a page's KV heads together; head-major
- * keeps each KV head's pages together.  Results are identical.  On MI355X
- * head-major streamed 11-20% faster for layers with 2 KV heads and 2-5% for
- * 16, was mixed for 4, and was 2-11% slower for 8.  The scales of fp8 pools are
- * [num_pages][num_kv_heads] in both. */
+ * keeps each KV head's pages together.  Results are identical.  Measured on
+ * one MI355X over 2.15 GB layers (4.3 GB fp8): head-major streamed 2% faster
+ * with 2 KV heads (bf16 and fp8), the same with 4 or 16, and 2% slower with 8.
+ * The scales of fp8 pools are [num_pages][num_kv_heads] in both. */
 enum { KF_KV_PAGE_MAJOR = 0, KF_KV_HEAD_MAJOR = 1 };
 
 enum {
