@@ -143,9 +143,9 @@ int kf_kv_append(const kf_shape* shape, void* k_pool, void* v_pool, float* k_sca
  * kf_partial_attn_workspace_bytes -- device scratch kf_partial_attn needs for
  * `num_routes` routes of at most `max_pages_per_route` pages each on the
  * current device (at least 256 bytes).  One workgroup handles a whole
- * (route, KV head) unit when there are enough units to fill the GPU; with
- * fewer, each unit is split over several workgroups whose partials go through
- * this workspace; a split launch of at least two rounds of resident
+ * (route, KV head) unit when the units fill the GPU evenly; otherwise each
+ * unit is split over several workgroups whose partials go through this
+ * workspace; a split launch of at least two rounds of resident
  * workgroups also keeps its dispatch order there (8 bytes per work item, a
  * table that a one-workgroup kernel writes before the partial kernel).  The
  * size covers every launch of at most `num_routes` routes, so a workspace
@@ -179,7 +179,9 @@ size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes
  * The plan reads the launch size, the KV heads and dtype, the device's
  * compute units, max_pages_per_route and shape->num_page_ids: a page table
  * under 90% of num_launch * max_pages_per_route marks the routes as ragged,
- * and ragged routes are cut into more ranges.  A max_pages_per_route far
+ * and ragged routes are cut into more ranges.  Equal units stay whole when
+ * they fill whole rounds of two per compute unit or spread evenly over the
+ * compute units (units mod CUs is 0 or at least 3/4 of the CUs).  A max_pages_per_route far
  * above the longest route therefore costs speed, never correctness.
  * Host only; launches nothing.  Any output pointer may be NULL.  Returns
  * KF_OK, KF_ERR_INVALID_ARG (null or invalid shape, negative sizes,

@@ -87,6 +87,21 @@ ChunkPlan plan_for_slots(int32_t num_routes, int32_t num_kv_heads, int32_t max_p
   // rounds would wait for its longest unit, so it is cut into ranges like
   // any other.
   if (units >= slots && units % slots == 0 && !ragged) return {whole, 1};
+  // Equal units that do not fill whole rounds still stay whole when they
+  // spread evenly over the compute units: every CU holds the same number of
+  // units, or all but at most a quarter of the CUs hold one more (units mod
+  // CUs is 0 or at least 3/4 of the CUs).  A CU streams about as fast with
+  // one workgroup as with two, so the launch takes as long as its busiest
+  // CU.  Measured against ranges on one box (units of 512 bf16 or 1024 fp8
+  // pages): bf16 192 units -14%, 448 -10%, 704 -6%, 768 -3%, 960 -5%; fp8
+  // 256 -11%, 448 -8%, 704 -5%, 768 -9%, 960 -6%.  Where a quarter to a half
+  // of the CUs would hold one unit more (320, 384, 576, 832 units) whole
+  // units were 3-15% slower than ranges.
+  const int64_t cus = slots / 2;
+  if (!ragged && units * 4 >= cus * 3) {
+    const int64_t rem = units % cus;
+    if (rem == 0 || rem * 4 >= cus * 3) return {whole, 1};
+  }
   // Fewer units than slots: units of equal length run best as about one
   // range per slot, one round of workgroups; ragged routes need more ranges
   // for the dispatcher to balance.  More units than slots: about 12 ranges
@@ -146,15 +161,22 @@ ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_page
 // workgroup, one workgroup per CU.  Both units of a CU then start at once:
 // with 256-thread workgroups the second workgroup of each CU started ~3 us
 // after the first, and the Llama layer ran 1.2-1.4% slower.  Units of 16384
-// pages ran 1.1% slower in this mode.  Launches over a route list keep one
-// unit per workgroup: they are made to run beside another launch, and a
-// 512-thread workgroup needs the registers of a whole CU, so it waits until
-// the other launch has left one entirely (the agentic query-first step took
-// 1402 us this way against 1257 us).
+// pages ran 1.1% slower in this mode.  Pairs go to CUs whole, so the busiest
+// CU holds 2 * ceil(units / (2 * CUs)) units against ceil(units / CUs) with
+// one unit per workgroup: units of more than 16 pages are paired only when
+// ceil(units / CUs) is even (768 units of 512 pages: 538 us paired against
+// 470 us single; 1280 units: 845 against 786).  Launches over a route list
+// keep one unit per workgroup: they are made to run beside another launch,
+// and a 512-thread workgroup needs the registers of a whole CU, so it waits
+// until the other launch has left one entirely (the agentic query-first
+// step took 1402 us this way against 1257 us).
 int32_t units_per_workgroup(bool fp8, bool route_list, const ChunkPlan& plan, int32_t num_launch,
                             int32_t num_kv_heads, int32_t max_pages_per_route) {
+  const int64_t cus = cu_count();
+  const int64_t units = (int64_t)num_launch * num_kv_heads;
+  const bool pairs_balance = max_pages_per_route <= kMinSplitPages || ((units + cus - 1) / cus) % 2 == 0;
   return !fp8 && !route_list && plan.max_chunks == 1 && max_pages_per_route <= kMaxPagesTwoUnit &&
-                 (int64_t)num_launch * num_kv_heads >= 2 * (int64_t)cu_count()
+                 units >= 2 * cus && pairs_balance
              ? 2
              : 1;
 }

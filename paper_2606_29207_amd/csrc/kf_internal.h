@@ -99,11 +99,13 @@ struct WorkspaceLayout {
 
 // How the pages of each (route, KV head) unit are spread over workgroups.
 // One workgroup owns a whole unit when the units fill whole rounds of the
-// GPU's resident workgroups (two per compute unit); otherwise units are cut
-// into chunks of chunk_pages pages, so the dispatcher balances uneven routes,
-// and a combine kernel follows: about 12 chunks per resident slot (6 for
-// fp8) when units outnumber slots, else about one (four when the page table shows ragged
-// routes), an odd number of chunks for the longest unit where it matters.
+// GPU's resident workgroups (two per compute unit), or, with equal routes,
+// when they spread evenly over the compute units (units mod CUs is 0 or at
+// least 3/4 of the CUs); otherwise units are cut into chunks of chunk_pages
+// pages, so the dispatcher balances them, and a combine kernel follows:
+// about 12 chunks per resident slot (6 for fp8) when units outnumber slots,
+// else about one (four when the page table shows ragged routes), an odd
+// number of chunks for the longest unit where it matters.
 struct ChunkPlan {
   int32_t chunk_pages, max_chunks;
 };

@@ -182,7 +182,9 @@ def _workspace_need(units_routes, H, G, maxp, ragged, slots=512, fp8=False):
     """Bytes one launch of `units_routes` routes needs, by the planner's rule:
     units that fill whole rounds of the resident slots stay whole (no
     records) unless the routes are ragged (a page table under 90% of routes
-    x max pages); otherwise chunks of about 12 per slot (more units than
+    x max pages), and so do equal units spread evenly over the compute units
+    (units mod CUs is 0 or at least 3/4 of the CUs, with at least 3/4 of a
+    unit per CU); otherwise chunks of about 12 per slot (more units than
     slots, never under 256 pages; 6 for fp8 pools) or about one per slot
     (fewer; four when ragged), never under 16 pages, an odd chunk count for the longest unit except for one per slot;
     records of (max, sum) and o per query head, and, for a split launch of
@@ -192,6 +194,9 @@ def _workspace_need(units_routes, H, G, maxp, ragged, slots=512, fp8=False):
     rup = lambda x: -(-x // 256) * 256  # noqa: E731
     units = units_routes * H
     if units == 0 or maxp <= 16 or (units >= slots and units % slots == 0 and not ragged):
+        return 256
+    cus = slots // 2
+    if not ragged and units * 4 >= cus * 3 and (units % cus == 0 or units % cus * 4 >= cus * 3):
         return 256
     target = ((6 if fp8 else 12) if units >= slots else 4 if ragged else 1) * slots
     c = max(-(-units * maxp // target), 16)
@@ -226,7 +231,9 @@ def test_workspace_bytes(lib):
         assert sizes[m] == max(need(k, 513) for k in range(0, m + 1))
     assert _workspace_need(64, 8, 4, 513, False) == 256           # 512 equal units: unsplit
     assert _workspace_need(64, 8, 4, 513, True) > 256             # ... ragged ones are cut
-    assert _workspace_need(63, 8, 4, 513, False) > 256            # 63 routes split either way
+    assert _workspace_need(63, 8, 4, 513, False) == 256           # 504 equal units: unsplit
+    assert _workspace_need(63, 8, 4, 513, True) > 256             # ... ragged ones are cut
+    assert _workspace_need(40, 8, 4, 513, False) > 256            # 320 equal units are cut
     # 1 sequence, 2 routes of 128 pages, 2 KV heads: 8 splits of 16 pages
     s = _shape(num_seqs=1, num_q_heads=8, num_kv_heads=2, num_pages=256, num_page_ids=256)
     recs = 2 * 2 * 8 * 4
@@ -282,8 +289,12 @@ def test_partial_attn_plan(lib):
     # the same 128 routes in a page table of 40000 (31%): ragged, so ranges
     c, m, u = plan(s, 128, 1024)
     assert m > 1 and m % 2 == 1 and u == 1 and c * m >= 1024
-    c, m, u = plan(s, 63, 516)                              # 504 units: split, combine launch
-    assert m > 1 and u == 1 and c * m >= 516 and c * (m - 1) < 516
+    assert plan(s, 63, 516) == (516, 1, 1)                  # 504 units: all but 8 CUs hold two
+    c, m, u = plan(s, 40, 516)                              # 320 units: a quarter of the CUs
+    assert m > 1 and u == 1 and c * m >= 516 and c * (m - 1) < 516   # would hold two: split
+    assert plan(big, 96, 516) == (516, 1, 1)                # 768 units, three per CU: pairs
+    assert plan(big, 120, 516) == (516, 1, 2)               # would leave a CU four; 960 units
+    assert plan(big, 88, 516) == (516, 1, 1)                # 704 units: three on 3/4 of the CUs
     fp8 = _shape(num_seqs=32, num_q_heads=64, num_kv_heads=8, kv_dtype=kf.KV_FP8_E4M3,
                  num_pages=131072, num_page_ids=131072)
     assert plan(fp8, 128, 1024) == (1024, 1, 1)
@@ -392,6 +403,9 @@ def test_plan_invariants_over_random_shapes(lib):
             assert m % 2 == 1, (units, maxp, pids, c, m)
         if u == 2:
             assert m == 1 and dtype == kf.KV_BF16 and not listed and units >= 512 and maxp <= 2048
+            assert maxp <= 16 or -(-units // 256) % 2 == 0
+        if not ragged and maxp > 16 and units * 4 >= 768 and (units % 256 == 0 or units % 256 >= 192):
+            assert m == 1, (units, maxp, pids, c, m)
         need = 256 if m == 1 else -(-units * m * group * 2 * 4 // 256) * 256 + \
             -(-units * m * group * 128 * 4 // 256) * 256
         if routes <= 200:   # the sizing loop is linear in the table's routes
