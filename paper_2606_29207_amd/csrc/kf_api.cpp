@@ -110,6 +110,21 @@ ChunkPlan plan_for_slots(int32_t num_routes, int32_t num_kv_heads, int32_t max_p
   // worth of units on, every unit is one range.
   const int64_t many = ranges_per_slot(fp8);
   if (units >= many * slots) return {whole, 1};
+  // Equal units that do not spread evenly whole, at least one per CU: the
+  // fewest ranges per unit whose work items do (units * ranges mod CUs is 0
+  // or at least 3/4 of the CUs), ranges of at least kMinSplitPages pages.
+  // Against the slot-count rule below (one box, units of 512 bf16 or 1024
+  // fp8 pages): bf16 320 units -9%, 416 -11%; fp8 320 -6%, 576 -2%, 640 -3%,
+  // 832 -1%; nowhere more than 0.5% slower.
+  if (!ragged && units >= cus) {
+    for (int64_t m = 2; m <= 16; ++m) {
+      const int64_t c = (max_pages_per_route + m - 1) / m;
+      if (c < kMinSplitPages) break;
+      if ((max_pages_per_route + c - 1) / c != m) continue;
+      const int64_t rem = units * m % cus;
+      if (rem == 0 || rem * 4 >= cus * 3) return {(int32_t)c, (int32_t)m};
+    }
+  }
   const int64_t target = (units < slots ? (ragged ? 4 : 1) : many) * slots;
   int64_t c = (units * max_pages_per_route + target - 1) / target;  // < 2^31 * 2^15
   if (c < kMinSplitPages) c = kMinSplitPages;

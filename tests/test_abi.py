@@ -184,7 +184,9 @@ def _workspace_need(units_routes, H, G, maxp, ragged, slots=512, fp8=False):
     records) unless the routes are ragged (a page table under 90% of routes
     x max pages), and so do equal units spread evenly over the compute units
     (units mod CUs is 0 or at least 3/4 of the CUs, with at least 3/4 of a
-    unit per CU); otherwise chunks of about 12 per slot (more units than
+    unit per CU); equal units, at least one per CU, otherwise take the fewest
+    ranges per unit (2 to 16, of at least 16 pages) whose work items spread
+    evenly so; otherwise chunks of about 12 per slot (more units than
     slots, never under 256 pages; 6 for fp8 pools) or about one per slot
     (fewer; four when ragged), never under 16 pages, an odd chunk count for the longest unit except for one per slot;
     records of (max, sum) and o per query head, and, for a split launch of
@@ -196,8 +198,22 @@ def _workspace_need(units_routes, H, G, maxp, ragged, slots=512, fp8=False):
     if units == 0 or maxp <= 16 or (units >= slots and units % slots == 0 and not ragged):
         return 256
     cus = slots // 2
-    if not ragged and units * 4 >= cus * 3 and (units % cus == 0 or units % cus * 4 >= cus * 3):
+    even = lambda n: n % cus == 0 or n % cus * 4 >= cus * 3  # noqa: E731
+    if not ragged and units * 4 >= cus * 3 and even(units):
         return 256
+    m = 0
+    if not ragged and cus <= units < (6 if fp8 else 12) * slots:
+        for mm in range(2, 17):            # the fewest ranges whose items spread evenly
+            c = -(-maxp // mm)
+            if c < 16:
+                break
+            if -(-maxp // c) == mm and even(units * mm):
+                m = mm
+                break
+    if m:
+        recs, items = units * m * G, units * m
+        ordered = 2 * slots <= items <= 1 << 20
+        return rup(recs * 2 * 4) + rup(recs * 128 * 4) + (rup((2 + 2 * items) * 4) if ordered else 0)
     target = ((6 if fp8 else 12) if units >= slots else 4 if ragged else 1) * slots
     c = max(-(-units * maxp // target), 16)
     if units >= slots and not fp8:
@@ -299,12 +315,16 @@ def test_partial_attn_plan(lib):
                  num_pages=131072, num_page_ids=131072)
     assert plan(fp8, 128, 1024) == (1024, 1, 1)
     fp8t = _shape(num_seqs=20, num_q_heads=64, num_kv_heads=8, kv_dtype=kf.KV_FP8_E4M3,
-                  num_pages=81920, num_page_ids=81920)
+                  num_pages=81920, num_page_ids=60000)
     bf16t = _shape(num_seqs=20, num_q_heads=64, num_kv_heads=8, num_pages=81920,
-                   num_page_ids=81920)
-    assert plan(fp8t, 80, 1024) == (214, 5, 1)               # 640 units: ~6 ranges per slot
+                   num_page_ids=60000)
+    assert plan(fp8t, 80, 1024) == (214, 5, 1)               # 640 ragged units: ~6 ranges per slot
     assert plan(bf16t, 80, 1024) == (205, 5, 1)             # ... and ~12 for bf16, but ranges
     #                                                         of >= 256 pages (then an odd count)
+    fp8e = _shape(num_seqs=20, num_q_heads=64, num_kv_heads=8, kv_dtype=kf.KV_FP8_E4M3,
+                  num_pages=81920, num_page_ids=81920)
+    assert plan(fp8e, 80, 1024) == (512, 2, 1)               # 640 equal units: 2 ranges, 5 per CU
+    assert plan(fp8e, 40, 1024) == (342, 3, 1)               # 320 equal units: 3 ranges, 3.75 per CU
     for pids in (100, 81920):
         sh = _shape(num_seqs=20, num_q_heads=64, num_kv_heads=8, kv_dtype=kf.KV_FP8_E4M3,
                     num_pages=10, num_page_ids=pids)
@@ -315,7 +335,7 @@ def test_partial_attn_plan(lib):
     assert plan(ragged, 48, 1024) == (147, 7, 1)            # 384 units, table at 73%: ~4 per slot
     equal = _shape(num_seqs=24, num_q_heads=32, num_kv_heads=8, num_pages=49152,
                    num_page_ids=49152)
-    assert plan(equal, 48, 1024) == (768, 2, 1)             # full table: one round
+    assert plan(equal, 48, 1024) == (512, 2, 1)             # full table: 384 units, 2 ranges (3 per CU)
     tiny = _shape(num_seqs=1, num_q_heads=8, num_kv_heads=2, num_pages=256, num_page_ids=256)
     assert plan(tiny, 2, 128) == (16, 8, 1)                 # 4 units: 8 splits of 16 pages
     assert plan(tiny, 2, 16) == (16, 1, 1)                  # too short to split
@@ -377,7 +397,8 @@ def test_plan_invariants_over_random_shapes(lib):
     """Planner invariants for 3000 seeded random launches (256 compute units
     assumed): the ranges cover the longest unit, no range is under 16 pages
     unless the unit stays whole, the range count is odd when units outnumber
-    slots or the routes are ragged (unless ranges hit the 16-page floor), two
+    slots or the routes are ragged (unless ranges hit the 16-page floor, or
+    equal units take the fewest ranges that spread evenly over the CUs), two
     units per workgroup only for unsplit bf16 launches over the whole table,
     and the workspace sized for the table covers the launch under any page
     table size."""
@@ -399,8 +420,13 @@ def test_plan_invariants_over_random_shapes(lib):
         assert m == 1 or c >= 16
         units = launch * hkv
         ragged = pids * 10 < launch * maxp * 9
+        spread = lambda n: n % 256 == 0 or n % 256 >= 192  # noqa: E731
         if m > 1 and (units >= 512 or ragged) and c > 16:
-            assert m % 2 == 1, (units, maxp, pids, c, m)
+            assert m % 2 == 1 or (not ragged and spread(units * m)), (units, maxp, pids, c, m)
+        if m > 1 and not ragged and units >= 256:   # equal units: the fewest evenly spread ranges
+            fits = [k for k in range(2, 17) if -(-maxp // k) >= 16 and
+                    -(-maxp // -(-maxp // k)) == k and spread(units * k)]
+            assert (fits and m == fits[0]) or not fits, (units, maxp, pids, c, m)
         if u == 2:
             assert m == 1 and dtype == kf.KV_BF16 and not listed and units >= 512 and maxp <= 2048
             assert maxp <= 16 or -(-units // 256) % 2 == 0
@@ -416,12 +442,12 @@ def test_no_alloc_step_refuses_launches_beyond_its_scratch(lib):
     """kf_decode_step_no_alloc checks every argument first, then refuses a
     launch whose split units need more than KF_SCRATCH_BYTES of scratch,
     before anything is launched: 200 routes x 8 KV heads x a group of 16, up
-    to 1000 pages, split into 5 ranges, need 66.6 MB."""
+    to 1000 pages, split into 3 ranges, need 40.0 MB."""
     from paper_2606_29207_amd import kf as k
     assert k.SCRATCH_BYTES == 32 << 20
     s = _shape(num_seqs=16, num_q_heads=128, num_kv_heads=8, num_pages=10 ** 6,
                num_page_ids=200 * 1000)
-    assert k.partial_attn_plan(s, 200, 1000)[1] == 5
+    assert k.partial_attn_plan(s, 200, 1000)[1] == 3
     v = lambda x: ctypes.c_void_p(x)  # noqa: E731
     args = [ctypes.byref(s), v(FAKE), v(FAKE), v(FAKE), None, None, v(FAKE), v(FAKE), v(FAKE), 200,
             v(FAKE), 1000, v(FAKE), v(FAKE), v(FAKE), v(FAKE), v(FAKE), v(FAKE), v(FAKE), None]
