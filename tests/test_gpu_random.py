@@ -79,22 +79,24 @@ def test_full_round_of_units_ragged_or_equal(gpu, ragged):
     compare_all(host(run_gpu(inst, 2, fused=True)), o)
 
 
-@pytest.mark.parametrize("num_seqs,pairs", [(56, False), (96, False), (120, True)])
-def test_equal_units_spread_over_the_cus_stay_whole(gpu, num_seqs, pairs):
+@pytest.mark.parametrize("num_seqs,tokens,plan_tail", [(56, 700, (1, 1)), (96, 700, (1, 1)),
+                                                      (120, 700, (1, 2)), (40, 1400, (3, 1))])
+def test_equal_units_spread_over_the_cus(gpu, num_seqs, tokens, plan_tail):
     """Equal routes whose (route, KV head) units do not fill whole rounds of
     the resident slots but spread evenly over the compute units (448, 768
     and 960 units on 256 CUs) stay whole: one unit per workgroup, or two
-    where pairs leave every CU an even count (960).  They match the oracle
-    over fused steps."""
+    where pairs leave every CU an even count (960).  320 units take the
+    fewest ranges whose work items spread evenly (3: 960 items).  They match
+    the oracle over fused steps."""
     import torch
     from paper_2606_29207_amd import kf
     from paper_2606_29207_amd.step import DecodeState
     wl = workload("llama8b_32k", num_seqs=num_seqs, part_tokens=1 << 20, appends=1)
-    inst = make_instance(wl, seed=37, steps=2, seq_lens=[700] * num_seqs)
+    inst = make_instance(wl, seed=37, steps=2, seq_lens=[tokens] * num_seqs)
     st = DecodeState.from_instance(inst)
     plan = kf.partial_attn_plan(st.shape, st.routes.shape[0], st.max_pages_per_route)
     if torch.cuda.get_device_properties(0).multi_processor_count == 256:
-        assert plan[1:] == (1, 2 if pairs else 1), plan
+        assert plan[1:] == plan_tail, plan
     del st
     o = run_oracle(inst, 2)
     compare_all(host(run_gpu(inst, 2, fused=True)), o)
