@@ -110,17 +110,18 @@ ChunkPlan plan_for_slots(int32_t num_routes, int32_t num_kv_heads, int32_t max_p
   // worth of units on, every unit is one range.
   const int64_t many = ranges_per_slot(fp8);
   if (units >= many * slots) return {whole, 1};
-  // Equal units that do not spread evenly whole, at least one per CU: the
-  // fewest ranges per unit whose work items do (units * ranges mod CUs is 0
-  // or at least 3/4 of the CUs), ranges of at least kMinSplitPages pages.
+  // Other equal units: the fewest ranges per unit (2 to 16, of at least
+  // kMinSplitPages pages) that give at least two work items per CU spread
+  // evenly over the CUs (items mod CUs is 0 or at least 3/4 of the CUs).
   // Against the slot-count rule below (one box, units of 512 bf16 or 1024
-  // fp8 pages): bf16 320 units -9%, 416 -11%; fp8 320 -6%, 576 -2%, 640 -3%,
-  // 832 -1%; nowhere more than 0.5% slower.
-  if (!ragged && units >= cus) {
+  // fp8 pages): bf16 96 units -16%, 160 -9%, 320 -9%, 416 -11%; fp8 96 -16%,
+  // 160 -2%, 320 -6%, 576 -2%, 640 -3%, 832 -1%; nowhere more than 0.9%
+  // slower.
+  if (!ragged) {
     for (int64_t m = 2; m <= 16; ++m) {
       const int64_t c = (max_pages_per_route + m - 1) / m;
       if (c < kMinSplitPages) break;
-      if ((max_pages_per_route + c - 1) / c != m) continue;
+      if ((max_pages_per_route + c - 1) / c != m || units * m < 2 * cus) continue;
       const int64_t rem = units * m % cus;
       if (rem == 0 || rem * 4 >= cus * 3) return {(int32_t)c, (int32_t)m};
     }

@@ -103,8 +103,8 @@ struct WorkspaceLayout {
 // when they spread evenly over the compute units (units mod CUs is 0 or at
 // least 3/4 of the CUs); otherwise units are cut into chunks of chunk_pages
 // pages, so the dispatcher balances them, and a combine kernel follows:
-// equal units, at least one per CU, take the fewest chunks whose work items
-// spread evenly so; other launches about 12 chunks per resident slot (6 for
+// other equal units take the fewest chunks giving at least two work items
+// per CU, spread evenly so; other launches about 12 chunks per resident slot (6 for
 // fp8) when units outnumber slots,
 // else about one (four when the page table shows ragged routes), an odd
 // number of chunks for the longest unit where it matters.

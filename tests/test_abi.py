@@ -184,9 +184,9 @@ def _workspace_need(units_routes, H, G, maxp, ragged, slots=512, fp8=False):
     records) unless the routes are ragged (a page table under 90% of routes
     x max pages), and so do equal units spread evenly over the compute units
     (units mod CUs is 0 or at least 3/4 of the CUs, with at least 3/4 of a
-    unit per CU); equal units, at least one per CU, otherwise take the fewest
-    ranges per unit (2 to 16, of at least 16 pages) whose work items spread
-    evenly so; otherwise chunks of about 12 per slot (more units than
+    unit per CU); other equal units take the fewest ranges per unit (2 to
+    16, of at least 16 pages) that give at least two work items per CU
+    spread evenly so; otherwise chunks of about 12 per slot (more units than
     slots, never under 256 pages; 6 for fp8 pools) or about one per slot
     (fewer; four when ragged), never under 16 pages, an odd chunk count for the longest unit except for one per slot;
     records of (max, sum) and o per query head, and, for a split launch of
@@ -202,12 +202,12 @@ def _workspace_need(units_routes, H, G, maxp, ragged, slots=512, fp8=False):
     if not ragged and units * 4 >= cus * 3 and even(units):
         return 256
     m = 0
-    if not ragged and cus <= units < (6 if fp8 else 12) * slots:
+    if not ragged and units < (6 if fp8 else 12) * slots:
         for mm in range(2, 17):            # the fewest ranges whose items spread evenly
             c = -(-maxp // mm)
             if c < 16:
                 break
-            if -(-maxp // c) == mm and even(units * mm):
+            if -(-maxp // c) == mm and units * mm >= slots and even(units * mm):
                 m = mm
                 break
     if m:
@@ -423,9 +423,9 @@ def test_plan_invariants_over_random_shapes(lib):
         spread = lambda n: n % 256 == 0 or n % 256 >= 192  # noqa: E731
         if m > 1 and (units >= 512 or ragged) and c > 16:
             assert m % 2 == 1 or (not ragged and spread(units * m)), (units, maxp, pids, c, m)
-        if m > 1 and not ragged and units >= 256:   # equal units: the fewest evenly spread ranges
+        if m > 1 and not ragged:   # equal units: the fewest evenly spread ranges
             fits = [k for k in range(2, 17) if -(-maxp // k) >= 16 and
-                    -(-maxp // -(-maxp // k)) == k and spread(units * k)]
+                    -(-maxp // -(-maxp // k)) == k and units * k >= 512 and spread(units * k)]
             assert (fits and m == fits[0]) or not fits, (units, maxp, pids, c, m)
         if u == 2:
             assert m == 1 and dtype == kf.KV_BF16 and not listed and units >= 512 and maxp <= 2048
