@@ -191,17 +191,31 @@ class BoundCall:
     ``stream`` (the current torch stream when None).  It holds a reference
     to every tensor it was bound to, so those pointers stay valid while the
     object lives: writes into the tensors between calls are seen; a tensor
-    replaced elsewhere is not.  A per-step decode loop pays the argument
-    checks once instead of on every step (tens of microseconds of host time
-    against a few microseconds of kernel time for small batches)."""
+    replaced elsewhere (or resized in place) is not.  The current device
+    must stay the tensors' device, and a given stream must belong to it.  A
+    per-step decode loop pays the argument checks once instead of on every
+    step (tens of microseconds of host time against a few microseconds of
+    kernel time for small batches)."""
 
-    __slots__ = ("_fn", "_what", "_args", "_keep")
+    __slots__ = ("_fn", "_what", "_args", "_keep", "_dev")
 
-    def __init__(self, fn, what: str, args, keep):
+    def __init__(self, fn, what: str, args, keep, device: int | None = None):
         self._fn, self._what, self._args, self._keep = fn, what, tuple(args), tuple(keep)
+        self._dev = device
+
+    def _handle(self, stream):
+        if self._dev is not None:
+            cur = _cur_device() if _cur_device is not None else torch.cuda.current_device()
+            if cur != self._dev or (stream is not None and stream.device_index != self._dev):
+                raise KFError(f"{self._what}: bound to cuda:{self._dev}, called with the current "
+                              f"device cuda:{cur}" + ("" if stream is None else
+                                                      f" and a stream of cuda:{stream.device_index}"))
+            if stream is None and _raw_stream is not None:
+                return _raw_stream(cur)
+        return _stream(stream)
 
     def __call__(self, stream=None):
-        st = self._fn(*self._args, _stream(stream))
+        st = self._fn(*self._args, self._handle(stream))
         if st != 0:
             _check(st, self._what)
 
@@ -213,8 +227,8 @@ class BoundTokenCall(BoundCall):
 
     __slots__ = ("_tok_at", "_tok_shape")
 
-    def __init__(self, fn, what: str, args, keep, tok_at: int, tok_shape):
-        super().__init__(fn, what, args, keep)
+    def __init__(self, fn, what: str, args, keep, tok_at: int, tok_shape, device=None):
+        super().__init__(fn, what, args, keep, device)
         self._tok_at, self._tok_shape = tok_at, torch.Size(tok_shape)
 
     def __call__(self, k_new, v_new, stream=None):
@@ -224,7 +238,7 @@ class BoundTokenCall(BoundCall):
                 raise KFError(f"{n} must be a contiguous bf16 device tensor "
                               f"{list(self._tok_shape)}")
         i, a = self._tok_at, self._args
-        st = self._fn(*a[:i], k_new.data_ptr(), v_new.data_ptr(), *a[i:], _stream(stream))
+        st = self._fn(*a[:i], k_new.data_ptr(), v_new.data_ptr(), *a[i:], self._handle(stream))
         if st != 0:
             _check(st, self._what)
 
@@ -267,7 +281,7 @@ def bind_kv_append(shape: Shape, k_pool, v_pool, routes, tail_route, page_ids, e
             _ptr(routes), routes.shape[0], _ptr(tail_route), _ptr(page_ids), _ptr(err_flags))
     return BoundTokenCall(lib.kf_kv_append, "kf_kv_append", args,
                           (sh, k_pool, v_pool, k_scale, v_scale, routes, tail_route, page_ids,
-                           err_flags), 5, (B, H, HEAD_DIM))
+                           err_flags), 5, (B, H, HEAD_DIM), k_pool.device.index)
 
 
 def kv_append(shape: Shape, k_pool, v_pool, k_new, v_new, routes, tail_route, page_ids,
@@ -331,11 +345,12 @@ def bind_partial_attn(shape: Shape, q, k_pool, v_pool, routes, max_pages_per_rou
     keep = (sh, q, k_pool, v_pool, k_scale, v_scale, routes, page_ids, o_part, lse_part,
             workspace, err_flags)
     if route_list is None:
-        return BoundCall(lib.kf_partial_attn, "kf_partial_attn", head + tail, keep)
+        return BoundCall(lib.kf_partial_attn, "kf_partial_attn", head + tail, keep, q.device.index)
     _dev(route_list, "route_list")
     _need(route_list.dtype == torch.int32 and route_list.dim() == 1, "route_list must be int32 [n]")
     return BoundCall(lib.kf_partial_attn_subset, "kf_partial_attn_subset",
-                     head + (_ptr(route_list), route_list.numel()) + tail, keep + (route_list,))
+                     head + (_ptr(route_list), route_list.numel()) + tail, keep + (route_list,),
+                     q.device.index)
 
 
 def partial_attn(shape: Shape, q, k_pool, v_pool, routes, max_pages_per_route, page_ids,
@@ -366,7 +381,8 @@ def bind_merge_partials(num_seqs, o_part, lse_part, seq_route_begin, out, lse_ou
     args = (int(num_seqs), R, Hq, D, _ptr(o_part), _ptr(lse_part), _ptr(seq_route_begin),
             _ptr(out), _ptr(lse_out), _ptr(err_flags))
     return BoundCall(lib.kf_merge_partials, "kf_merge_partials", args,
-                     (o_part, lse_part, seq_route_begin, out, lse_out, err_flags))
+                     (o_part, lse_part, seq_route_begin, out, lse_out, err_flags),
+                     o_part.device.index)
 
 
 def merge_partials(num_seqs, o_part, lse_part, seq_route_begin, out, lse_out, err_flags,
@@ -408,10 +424,11 @@ def bind_decode_step(shape: Shape, q, k_pool, v_pool, routes, tail_route, max_pa
             seq_route_begin, o_part, lse_part, out, lse_out, err_flags)
     if workspace is None:
         return BoundTokenCall(lib.kf_decode_step_no_alloc, "kf_decode_step_no_alloc",
-                              args + (_ptr(err_flags),), keep, 6, (B, H, HEAD_DIM))
+                              args + (_ptr(err_flags),), keep, 6, (B, H, HEAD_DIM), q.device.index)
     return BoundTokenCall(lib.kf_decode_step, "kf_decode_step",
                           args + (_ptr(workspace), workspace.numel() * workspace.element_size(),
-                                  _ptr(err_flags)), keep + (workspace,), 6, (B, H, HEAD_DIM))
+                                  _ptr(err_flags)), keep + (workspace,), 6, (B, H, HEAD_DIM),
+                          q.device.index)
 
 
 def decode_step(shape: Shape, q, k_pool, v_pool, k_new, v_new, routes, tail_route,

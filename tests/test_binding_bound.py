@@ -12,6 +12,7 @@ from paper_2606_29207_amd import kf  # noqa: E402
 
 class _Stream:
     cuda_stream = 0xABC
+    device_index = 0
 
 
 def test_bound_call_appends_the_stream():
@@ -21,6 +22,23 @@ def test_bound_call_appends_the_stream():
     call(_Stream())
     assert len(seen) == 2
     assert seen[0][:3] == (1, 2, 3) and seen[0][3] == 0xABC
+
+
+def test_bound_call_refuses_another_device(monkeypatch):
+    """A call bound to cuda:1 refuses to run while cuda:0 is current, or on
+    a stream of another device, before calling the library."""
+    seen = []
+    monkeypatch.setattr(kf, "_cur_device", lambda: 0)
+    call = kf.BoundCall(lambda *a: seen.append(a) or 0, "kf_x", (1,), (), 1)
+    with pytest.raises(kf.KFError, match="bound to cuda:1"):
+        call(_Stream())
+    monkeypatch.setattr(kf, "_cur_device", lambda: 1)
+    with pytest.raises(kf.KFError, match="a stream of cuda:0"):
+        call(_Stream())
+    s1 = _Stream()
+    s1.device_index = 1
+    call(s1)
+    assert len(seen) == 1
 
 
 def test_bound_call_raises_on_a_status():
