@@ -183,7 +183,9 @@ size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes
  * they fill whole rounds of two per compute unit or spread evenly over the
  * compute units (units mod CUs is 0 or at least 3/4 of the CUs); other
  * equal units take the fewest ranges (up to 16) that give at least two work
- * items per compute unit, spread evenly so.  A max_pages_per_route far
+ * items per compute unit, spread evenly so.  Launches over a route list
+ * (route_list_launch = 1) skip these two rules: the page table does not
+ * tell whether a list's routes are equal.  A max_pages_per_route far
  * above the longest route therefore costs speed, never correctness.
  * Host only; launches nothing.  Any output pointer may be NULL.  Returns
  * KF_OK, KF_ERR_INVALID_ARG (null or invalid shape, negative sizes,

@@ -79,7 +79,7 @@ int64_t ranges_per_slot(bool fp8) { return fp8 ? 6 : 12; }
 namespace {
 // plan_chunks for a GPU with `slots` resident workgroups (two per CU).
 ChunkPlan plan_for_slots(int32_t num_routes, int32_t num_kv_heads, int32_t max_pages_per_route,
-                         bool ragged, bool fp8, int64_t slots) {
+                         bool ragged, bool fp8, int64_t slots, bool listed) {
   const int64_t units = (int64_t)num_routes * num_kv_heads;
   const int32_t whole = max_pages_per_route > 0 ? max_pages_per_route : 1;
   if (units <= 0 || max_pages_per_route <= kMinSplitPages) return {whole, 1};
@@ -87,6 +87,9 @@ ChunkPlan plan_for_slots(int32_t num_routes, int32_t num_kv_heads, int32_t max_p
   // rounds would wait for its longest unit, so it is cut into ranges like
   // any other.
   if (units >= slots && units % slots == 0 && !ragged) return {whole, 1};
+  // The rules for equal units below trust the page table's reading, which
+  // says nothing about the routes of a list (a part of a table), so
+  // route-list launches skip them.
   // Equal units that do not fill whole rounds still stay whole when they
   // spread evenly over the compute units: every CU holds the same number of
   // units, or all but at most a quarter of the CUs hold one more (units mod
@@ -98,7 +101,7 @@ ChunkPlan plan_for_slots(int32_t num_routes, int32_t num_kv_heads, int32_t max_p
   // of the CUs would hold one unit more (320, 384, 576, 832 units) whole
   // units were 3-15% slower than ranges.
   const int64_t cus = slots / 2;
-  if (!ragged && units * 4 >= cus * 3) {
+  if (!ragged && !listed && units * 4 >= cus * 3) {
     const int64_t rem = units % cus;
     if (rem == 0 || rem * 4 >= cus * 3) return {whole, 1};
   }
@@ -117,7 +120,7 @@ ChunkPlan plan_for_slots(int32_t num_routes, int32_t num_kv_heads, int32_t max_p
   // fp8 pages): bf16 96 units -16%, 160 -9%, 320 -9%, 416 -11%; fp8 96 -16%,
   // 160 -2%, 320 -6%, 576 -2%, 640 -3%, 832 -1%; nowhere more than 0.9%
   // slower.
-  if (!ragged) {
+  if (!ragged && !listed) {
     for (int64_t m = 2; m <= 16; ++m) {
       const int64_t c = (max_pages_per_route + m - 1) / m;
       if (c < kMinSplitPages) break;
@@ -167,9 +170,9 @@ ChunkPlan plan_for_slots(int32_t num_routes, int32_t num_kv_heads, int32_t max_p
 }  // namespace
 
 ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_pages_per_route,
-                      bool ragged, bool fp8) {
+                      bool ragged, bool fp8, bool listed) {
   return plan_for_slots(num_routes, num_kv_heads, max_pages_per_route, ragged, fp8,
-                        2 * (int64_t)cu_count());
+                        2 * (int64_t)cu_count(), listed);
 }
 
 // Unsplit bf16 launches over the whole table with at least two units per
@@ -247,23 +250,25 @@ size_t kf_partial_attn_workspace_bytes(const kf_shape* shape, int32_t num_routes
   // The largest need of any launch of at most num_routes routes: fewer routes
   // may not fill the GPU and then split their units, so a workspace sized for
   // a whole route table must also serve a launch over a subset of it.  Both
-  // readings of the page table (ragged routes or not) are covered, so the
-  // size does not depend on shape->num_page_ids, which grows with the table.
+  // readings of the page table (ragged routes or not) and both kinds of
+  // launch (over the table, over a route list) are covered, so the size does
+  // not depend on shape->num_page_ids, which grows with the table.
   // Launches whose units reach ranges_per_slot * slots keep every unit whole
   // and need no workspace, so at most that many route counts are visited.
   const int64_t slots = 2 * (int64_t)kf::cu_count();
   const int64_t split_units = kf::ranges_per_slot(fp8) * slots;
   size_t most = 256;
   for (int32_t m = 1; m <= num_routes && (int64_t)m * shape->num_kv_heads < split_units; ++m) {
-    for (const bool ragged : {false, true}) {
-      const kf::ChunkPlan plan =
-          kf::plan_for_slots(m, shape->num_kv_heads, max_pages_per_route, ragged, fp8, slots);
-      const size_t t =
-          kf::workspace_layout(m, shape->num_kv_heads, group, plan.max_chunks,
-                               kf::ordered_dispatch(plan, m, shape->num_kv_heads, slots))
-              .total;
-      if (t > most) most = t;
-    }
+    for (const bool ragged : {false, true})
+      for (const bool listed : {false, true}) {
+        const kf::ChunkPlan plan = kf::plan_for_slots(m, shape->num_kv_heads, max_pages_per_route,
+                                                      ragged, fp8, slots, listed);
+        const size_t t =
+            kf::workspace_layout(m, shape->num_kv_heads, group, plan.max_chunks,
+                                 kf::ordered_dispatch(plan, m, shape->num_kv_heads, slots))
+                .total;
+        if (t > most) most = t;
+      }
   }
   return most;
 }
@@ -279,7 +284,7 @@ int kf_partial_attn_plan(const kf_shape* shape, int32_t num_launch, int32_t max_
   const kf::ChunkPlan plan = kf::plan_chunks(
       num_launch, shape->num_kv_heads, max_pages_per_route,
       kf::ragged_table(shape->num_page_ids, num_launch, max_pages_per_route),
-      shape->kv_dtype == KF_KV_FP8_E4M3);
+      shape->kv_dtype == KF_KV_FP8_E4M3, route_list_launch == 1);
   if (chunk_pages) *chunk_pages = plan.chunk_pages;
   if (max_chunks) *max_chunks = plan.max_chunks;
   if (units_per_wg)
@@ -357,7 +362,7 @@ int prepare_partial(const kf_shape* shape, const void* q, const void* k_pool, co
   const kf::ChunkPlan plan = kf::plan_chunks(
       num_launch, shape->num_kv_heads, max_pages_per_route,
       kf::ragged_table(shape->num_page_ids, num_launch, max_pages_per_route),
-      shape->kv_dtype == KF_KV_FP8_E4M3);
+      shape->kv_dtype == KF_KV_FP8_E4M3, route_list != nullptr);
   const bool ordered =
       kf::ordered_dispatch(plan, num_launch, shape->num_kv_heads, 2 * (int64_t)kf::cu_count());
   const kf::WorkspaceLayout l =

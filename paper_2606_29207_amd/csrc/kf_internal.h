@@ -117,8 +117,11 @@ bool ragged_table(int64_t num_page_ids, int32_t num_routes, int32_t max_pages_pe
 // Ranges per resident slot when units outnumber slots (12 bf16, 6 fp8); from
 // that many units per slot on, every unit runs whole.
 int64_t ranges_per_slot(bool fp8);
+// listed: a launch over a route list (kf_partial_attn_subset), whose routes
+// the page table's reading does not describe; the equal-unit rules are
+// skipped for it.
 ChunkPlan plan_chunks(int32_t num_routes, int32_t num_kv_heads, int32_t max_pages_per_route,
-                      bool ragged, bool fp8);
+                      bool ragged, bool fp8, bool listed);
 // Units per workgroup of a partial-attention launch of num_launch routes
 // (1 or 2); route_list: a launch over a route list (kf_partial_attn_subset).
 int32_t units_per_workgroup(bool fp8, bool route_list, const ChunkPlan& plan, int32_t num_launch,

@@ -178,7 +178,7 @@ def test_merge_host_checks(lib):
     assert lib.kf_merge_partials(0, 4, 8, 128, *([None] * 7), None) == 0
 
 
-def _workspace_need(units_routes, H, G, maxp, ragged, slots=512, fp8=False):
+def _workspace_need(units_routes, H, G, maxp, ragged, slots=512, fp8=False, listed=False):
     """Bytes one launch of `units_routes` routes needs, by the planner's rule:
     units that fill whole rounds of the resident slots stay whole (no
     records) unless the routes are ragged (a page table under 90% of routes
@@ -186,7 +186,7 @@ def _workspace_need(units_routes, H, G, maxp, ragged, slots=512, fp8=False):
     (units mod CUs is 0 or at least 3/4 of the CUs, with at least 3/4 of a
     unit per CU); other equal units take the fewest ranges per unit (2 to
     16, of at least 16 pages) that give at least two work items per CU
-    spread evenly so; otherwise chunks of about 12 per slot (more units than
+    spread evenly so (not for route-list launches); otherwise chunks of about 12 per slot (more units than
     slots, never under 256 pages; 6 for fp8 pools) or about one per slot
     (fewer; four when ragged), never under 16 pages, an odd chunk count for the longest unit except for one per slot;
     records of (max, sum) and o per query head, and, for a split launch of
@@ -199,10 +199,10 @@ def _workspace_need(units_routes, H, G, maxp, ragged, slots=512, fp8=False):
         return 256
     cus = slots // 2
     even = lambda n: n % cus == 0 or n % cus * 4 >= cus * 3  # noqa: E731
-    if not ragged and units * 4 >= cus * 3 and even(units):
+    if not ragged and not listed and units * 4 >= cus * 3 and even(units):
         return 256
     m = 0
-    if not ragged and units < (6 if fp8 else 12) * slots:
+    if not ragged and not listed and units < (6 if fp8 else 12) * slots:
         for mm in range(2, 17):            # the fewest ranges whose items spread evenly
             c = -(-maxp // mm)
             if c < 16:
@@ -242,7 +242,8 @@ def test_workspace_bytes(lib):
     s = _shape(num_seqs=16, num_q_heads=32, num_kv_heads=8, num_pages=40000, num_page_ids=40000)
     sizes = [kf.partial_attn_workspace_bytes(s, m, 513) for m in range(0, 80)]
     assert all(a <= b for a, b in zip(sizes, sizes[1:]))            # non-decreasing
-    need = lambda k, maxp: max(_workspace_need(k, 8, 4, maxp, rg) for rg in (False, True))  # noqa: E731
+    need = lambda k, maxp: max(_workspace_need(k, 8, 4, maxp, rg, listed=ls)  # noqa: E731
+                               for rg in (False, True) for ls in (False, True))
     for m in range(0, 80):
         assert sizes[m] == max(need(k, 513) for k in range(0, m + 1))
     assert _workspace_need(64, 8, 4, 513, False) == 256           # 512 equal units: unsplit
@@ -306,6 +307,8 @@ def test_partial_attn_plan(lib):
     c, m, u = plan(s, 128, 1024)
     assert m > 1 and m % 2 == 1 and u == 1 and c * m >= 1024
     assert plan(s, 63, 516) == (516, 1, 1)                  # 504 units: all but 8 CUs hold two
+    c, m, u = plan(s, 63, 516, route_list=True)             # ... a list's routes may be ragged:
+    assert m == 2 and u == 1 and c * m >= 516               # about one range per slot
     c, m, u = plan(s, 40, 516)                              # 320 units: a quarter of the CUs
     assert m > 1 and u == 1 and c * m >= 516 and c * (m - 1) < 516   # would hold two: split
     assert plan(big, 96, 516) == (516, 1, 1)                # 768 units, three per CU: pairs
@@ -329,7 +332,8 @@ def test_partial_attn_plan(lib):
         sh = _shape(num_seqs=20, num_q_heads=64, num_kv_heads=8, kv_dtype=kf.KV_FP8_E4M3,
                     num_pages=10, num_page_ids=pids)
         assert kf.partial_attn_workspace_bytes(sh, 80, 1024) == max(
-            _workspace_need(k, 8, 8, 1024, rg, fp8=True) for k in range(81) for rg in (False, True))
+            _workspace_need(k, 8, 8, 1024, rg, fp8=True, listed=ls) for k in range(81)
+            for rg in (False, True) for ls in (False, True))
     ragged = _shape(num_seqs=24, num_q_heads=32, num_kv_heads=8, num_pages=36000,
                     num_page_ids=36000)
     assert plan(ragged, 48, 1024) == (147, 7, 1)            # 384 units, table at 73%: ~4 per slot
@@ -422,15 +426,17 @@ def test_plan_invariants_over_random_shapes(lib):
         ragged = pids * 10 < launch * maxp * 9
         spread = lambda n: n % 256 == 0 or n % 256 >= 192  # noqa: E731
         if m > 1 and (units >= 512 or ragged) and c > 16:
-            assert m % 2 == 1 or (not ragged and spread(units * m)), (units, maxp, pids, c, m)
-        if m > 1 and not ragged:   # equal units: the fewest evenly spread ranges
+            assert m % 2 == 1 or (not ragged and not listed and spread(units * m)), \
+                (units, maxp, pids, c, m)
+        if m > 1 and not ragged and not listed:   # equal units: the fewest evenly spread ranges
             fits = [k for k in range(2, 17) if -(-maxp // k) >= 16 and
                     -(-maxp // -(-maxp // k)) == k and units * k >= 512 and spread(units * k)]
             assert (fits and m == fits[0]) or not fits, (units, maxp, pids, c, m)
         if u == 2:
             assert m == 1 and dtype == kf.KV_BF16 and not listed and units >= 512 and maxp <= 2048
             assert maxp <= 16 or -(-units // 256) % 2 == 0
-        if not ragged and maxp > 16 and units * 4 >= 768 and (units % 256 == 0 or units % 256 >= 192):
+        if not ragged and not listed and maxp > 16 and units * 4 >= 768 and \
+                (units % 256 == 0 or units % 256 >= 192):
             assert m == 1, (units, maxp, pids, c, m)
         need = 256 if m == 1 else -(-units * m * group * 2 * 4 // 256) * 256 + \
             -(-units * m * group * 128 * 4 // 256) * 256
