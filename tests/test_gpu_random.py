@@ -4,7 +4,8 @@ included), route length, pool placement, appends and step count are all
 drawn from one generator per case.  Every fourth case draws many short
 routes, so that launches with at least 512 unsplit units (two units per
 workgroup for bf16) are among them; the others mostly split their units.
-The plan each case takes is checked to be a valid one."""
+The plan each case takes is checked to be a valid one.  A second set draws
+equal-length batches of 32 to 1100 units, for the planner's equal-unit rules."""
 import numpy as np
 import pytest
 
@@ -100,3 +101,32 @@ def test_equal_units_spread_over_the_cus(gpu, num_seqs, tokens, plan_tail):
     del st
     o = run_oracle(inst, 2)
     compare_all(host(run_gpu(inst, 2, fused=True)), o)
+
+
+def draw_equal(case):
+    """An equal-length batch: every sequence holds the same number of tokens,
+    split into routes of one drawn length, with 32 to 1100 (route, KV head)
+    units, so that the planner's rules for equal units (whole units spread
+    evenly over the CUs, the fewest evenly spread ranges, pairs per
+    workgroup) are all taken across the cases."""
+    rng = np.random.default_rng([7, 7, case])
+    fp8 = bool(rng.random() < 0.35)
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    group = int(rng.integers(1, 9))
+    L = int(rng.integers(200, 2500))
+    part = 16 * int(rng.integers(max(1, L // 16 // 4), L // 16 + 2))
+    units_target = int(rng.integers(32, 1100))
+    B = max(1, units_target // (-(-L // part) * hkv))
+    appends = int(rng.random() < 0.6)
+    over = dict(num_seqs=B, num_q_heads=group * hkv, num_kv_heads=hkv, part_tokens=part,
+                appends=appends, permuted=bool(rng.random() < 0.3))
+    wl = workload("wide_gqa_fp8" if fp8 else "llama8b_32k", **over)
+    steps = 2 if appends else 1
+    return make_instance(wl, seed=5000 + case, steps=steps, seq_lens=[L] * B), steps
+
+
+@pytest.mark.parametrize("case", range(24))
+def test_random_equal_shape(gpu, case):
+    inst, steps = draw_equal(case)
+    o = run_oracle(inst, steps)
+    compare_all(host(run_gpu(inst, steps, fused=bool(inst.wl.appends))), o)
