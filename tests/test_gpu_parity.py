@@ -46,6 +46,12 @@ CASES = {
     "fp8_g2": ("wide_gqa_fp8", dict(num_seqs=2, num_q_heads=8, num_kv_heads=4, part_tokens=1024), [2049, 700], 1),
     # many KV heads (32), each with a group of 2
     "hkv32_g2": ("llama8b_32k", dict(num_seqs=2, num_q_heads=64, num_kv_heads=32, part_tokens=1024), [1500, 530], 1),
+    # multi-head attention with 64 heads, and fp8 pools of 32 KV heads (scales [page][32]),
+    # both appending over fused steps
+    "mha_hkv64": ("llama8b_32k", dict(num_seqs=2, num_q_heads=64, num_kv_heads=64, part_tokens=512,
+                                      appends=1), [700, 90], 3),
+    "fp8_hkv32_g2": ("wide_gqa_fp8", dict(num_seqs=2, num_q_heads=64, num_kv_heads=32, part_tokens=768,
+                                          appends=1), [1600, 255], 3),
     # >= 512 (route, KV head) units: one workgroup per unit, no split
     "many_units": ("llama8b_32k", dict(part_tokens=256), [300 + 97 * i for i in range(16)], 2),
     # > 512 units, not a whole number of rounds, uneven routes: chunked units
