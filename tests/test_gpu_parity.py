@@ -58,6 +58,10 @@ CASES = {
     "chunked_uneven": ("llama8b_32k", dict(part_tokens=1024),
                        [1000 + 523 * i for i in range(16)], 1),
     "short_routes": ("llama8b_32k", dict(num_seqs=4, num_q_heads=8, num_kv_heads=2, part_tokens=16), [1, 15, 16, 33], 2),
+    # 1500 short sequences (0 to 99 tokens, routes of 64): thousands of routes, merge
+    # grid over 1500 sequences, appends into fresh and full pages
+    "many_seqs": ("llama8b_32k", dict(num_seqs=1500, num_q_heads=8, num_kv_heads=2, part_tokens=64,
+                                      appends=1), [(37 * i) % 100 for i in range(1500)], 2),
 }
 
 
